@@ -1,0 +1,173 @@
+/*
+ * Reference oracle for exact softmax attention and log-sum-exp merging.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the slow, obviously-correct CPU
+ * definition that the GPU kernels are checked against.  Only the test suite,
+ * the smoke check and the CPU-baseline leg of the benchmark may load it; the
+ * product library never links, calls or falls back to it, and it shares no
+ * source, header, table or helper with the GPU path.
+ *
+ * What is computed (paper, Sec. 3.5 "Multi-GPU unified sequence parallelism"):
+ *   Ulysses gives every GPU exact attention over the whole token sequence for
+ *   a subset of heads; Ring streams key/value blocks and combines them
+ *   "online-softmax" style; the parallel result equals single-device attention
+ *   up to reduction order.  The plain definition of that result, per batch b,
+ *   head h and query row i, with the caller's float32 scale widened to double:
+ *
+ *       s_j  = scale * sum_t Q[b,i,h,t] * K[b,j,h,t]          j = 0..Skv-1
+ *       m    = max_j s_j
+ *       l    = sum_j exp(s_j - m)
+ *       O[b,i,h,:]  = sum_j exp(s_j - m) * V[b,j,h,:] / l
+ *       LSE[b,h,i]  = m + log(l)                     (natural log)
+ *
+ *   This is written as two passes over each row (all scores first, then the
+ *   max, the sum and the weighted sum): deliberately NOT the blockwise online
+ *   recurrence the kernels use.  A key/value chunk's partial result is the same
+ *   function applied to that chunk's rows.
+ *
+ *   Merging n partial results (O_c, L_c) of disjoint key chunks back into the
+ *   result over their union is the log-sum-exp identity:
+ *       m* = max_c L_c,   L = m* + log sum_c exp(L_c - m*),
+ *       O  = sum_c exp(L_c - L) * O_c.
+ *   A part with L_c = -inf carries no keys and weight 0; if every part has
+ *   L_c = -inf the merged row is O = 0, L = -inf.
+ *
+ * Inputs are bf16 bit patterns (uint16), widened exactly to double.  Tensors
+ * are logical [B, S, H, D] with element strides for b, s and h, and D
+ * contiguous.  Outputs are double: O [B, Sq, H, D] contiguous, LSE [B, H, Sq].
+ * Rounding: every product and sum is done in double precision.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+static double bf16_to_double(uint16_t bits)
+{
+    /* a bf16 value is the top half of the float32 with the same bits */
+    uint32_t u = ((uint32_t)bits) << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+/* Exact attention over all Skv keys; returns 0 on success, -1 on bad sizes
+ * or allocation failure. */
+int oracle_attn(const uint16_t *q, int64_t q_sb, int64_t q_ss, int64_t q_sh,
+                const uint16_t *k, int64_t k_sb, int64_t k_ss, int64_t k_sh,
+                const uint16_t *v, int64_t v_sb, int64_t v_ss, int64_t v_sh,
+                double *o, double *lse,
+                int B, int H, int Sq, int Skv, int D, float scale_f32)
+{
+    if (B < 0 || H < 0 || Sq < 0 || Skv < 1 || D < 1)
+        return -1;
+    const double scale = (double)scale_f32;
+    int failed = 0;
+
+#pragma omp parallel
+    {
+        double *s = (double *)malloc(sizeof(double) * (size_t)Skv);
+        double *acc = (double *)malloc(sizeof(double) * (size_t)D);
+        if (!s || !acc) {
+#pragma omp atomic write
+            failed = 1;
+        }
+#pragma omp for collapse(3) schedule(dynamic, 4)
+        for (int b = 0; b < B; b++)
+            for (int h = 0; h < H; h++)
+                for (int i = 0; i < Sq; i++) {
+                    if (!s || !acc)
+                        continue;
+                    const uint16_t *qi = q + b * q_sb + i * q_ss + h * q_sh;
+                    /* pass 1: every scaled score of the row */
+                    for (int j = 0; j < Skv; j++) {
+                        const uint16_t *kj = k + b * k_sb + j * k_ss + h * k_sh;
+                        double dot = 0.0;
+                        for (int t = 0; t < D; t++)
+                            dot += bf16_to_double(qi[t]) * bf16_to_double(kj[t]);
+                        s[j] = scale * dot;
+                    }
+                    /* pass 2: max, normaliser and weighted sum of value rows */
+                    double m = -INFINITY;
+                    for (int j = 0; j < Skv; j++)
+                        if (s[j] > m)
+                            m = s[j];
+                    double l = 0.0;
+                    for (int t = 0; t < D; t++)
+                        acc[t] = 0.0;
+                    for (int j = 0; j < Skv; j++) {
+                        const double p = exp(s[j] - m);
+                        const uint16_t *vj = v + b * v_sb + j * v_ss + h * v_sh;
+                        l += p;
+                        for (int t = 0; t < D; t++)
+                            acc[t] += p * bf16_to_double(vj[t]);
+                    }
+                    double *oi = o + (((int64_t)b * Sq + i) * H + h) * D;
+                    for (int t = 0; t < D; t++)
+                        oi[t] = acc[t] / l;
+                    lse[((int64_t)b * H + h) * Sq + i] = m + log(l);
+                }
+        free(s);
+        free(acc);
+    }
+    return failed ? -1 : 0;
+}
+
+/* Log-sum-exp merge of num_parts partial results of disjoint key chunks.
+ * o_parts[c]: [B, Sq, H, D] contiguous; lse_parts[c]: [B, H, Sq]. */
+int oracle_merge(const double *const *o_parts, const double *const *lse_parts,
+                 int num_parts, double *o, double *lse,
+                 int B, int H, int Sq, int D)
+{
+    if (num_parts < 1 || B < 0 || H < 0 || Sq < 0 || D < 1)
+        return -1;
+#pragma omp parallel for collapse(3) schedule(static)
+    for (int b = 0; b < B; b++)
+        for (int h = 0; h < H; h++)
+            for (int i = 0; i < Sq; i++) {
+                const int64_t li = ((int64_t)b * H + h) * Sq + i;
+                const int64_t oi = (((int64_t)b * Sq + i) * H + h) * D;
+                double mstar = -INFINITY;
+                for (int c = 0; c < num_parts; c++)
+                    if (lse_parts[c][li] > mstar)
+                        mstar = lse_parts[c][li];
+                if (mstar == -INFINITY) {
+                    /* no part holds any key: the empty-set result */
+                    for (int t = 0; t < D; t++)
+                        o[oi + t] = 0.0;
+                    lse[li] = -INFINITY;
+                    continue;
+                }
+                double sum = 0.0;
+                for (int c = 0; c < num_parts; c++)
+                    sum += exp(lse_parts[c][li] - mstar);
+                const double L = mstar + log(sum);
+                for (int t = 0; t < D; t++) {
+                    double acc = 0.0;
+                    for (int c = 0; c < num_parts; c++) {
+                        const double w = exp(lse_parts[c][li] - L);
+                        acc += w * o_parts[c][oi + t];
+                    }
+                    o[oi + t] = acc;
+                }
+                lse[li] = L;
+            }
+    return 0;
+}
+
+/* Number of OpenMP threads the oracle runs on (reported next to its timing). */
+int oracle_num_threads(void)
+{
+    int n = 1;
+#pragma omp parallel
+    {
+#pragma omp single
+        {
+#ifdef _OPENMP
+            extern int omp_get_num_threads(void);
+            n = omp_get_num_threads();
+#endif
+        }
+    }
+    return n;
+}
