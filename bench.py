@@ -1,0 +1,221 @@
+#!/usr/bin/env python3
+"""Throughput of the window-attention hot path on one MI355X.
+
+One step = one pass of the whole hot path over one synthetic batch:
+  self   exact self-attention of a 25-frame window: B=1, H=12, S=10920
+         (7 latent frames x 30 x 52 patches), d=128, bf16 O + fp32 LSE
+  cross  cross-attention of those 10920 queries to 512 conditioning tokens
+  share  one sequence-parallel rank's share: H=5, Sq=10920, keys in 4
+         contiguous chunks of 2730 -> 4 partials (fp32 O + LSE) -> LSE merge
+         into bf16 O
+Inputs are resident in HBM before the timed region.  `value` is the step's
+algorithmic attention FLOPs (4*B*H*Sq*Skv*d per attention call, softmax and
+padding excluded) divided by the step time.  Prints ONE JSON line.
+"""
+import argparse
+import json
+import math
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+REPO = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, REPO)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+WINDOW = dict(B=1, H=12, S=10920, D=128, ctx=512, seed=3)
+SHARE = dict(B=1, H=5, S=10920, D=128, chunks=4, seed=4)
+
+
+def attn_flops(B, H, Sq, Skv, D):
+    return 4.0 * B * H * Sq * Skv * D
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor()
+
+
+def cpu_baseline(target_s: float):
+    """Times the fp64 oracle on a bounded sample of the window self-attention:
+    a few query rows of all 12 heads against all 10920 keys."""
+    import oracle
+    from paper_2607_28144_amd import synth
+    W = WINDOW
+    q, k, v = synth.qkv(W["seed"], W["B"], W["H"], W["S"], W["S"], W["D"])
+    scale = synth.default_scale(W["D"])
+    rows = 8
+    while True:
+        qs = np.ascontiguousarray(q[:, :rows])
+        t0 = time.perf_counter()
+        oracle.attn(qs, k, v, scale)
+        dt = time.perf_counter() - t0
+        if dt >= target_s or rows >= W["S"]:
+            break
+        rows = min(W["S"], max(rows * 2, int(rows * target_s / max(dt, 1e-3) * 1.1)))
+    flops = attn_flops(W["B"], W["H"], rows, W["S"], W["D"])
+    return {
+        "value": flops / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": f"window self-attention, {rows} query rows x {W['H']} heads x {W['S']} keys, d={W['D']} "
+                  f"(fp64 two-pass oracle, {dt:.1f} s on {cpu_model()})",
+        "seconds": dt,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--only", choices=["self", "cross", "share"], default=None,
+                    help="time one component alone (for profiling)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle sample")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on one GPU only; --gpus must be 1 (the multi-GPU sharding is a "
+              "design, not part of this build)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_28144_amd import api, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def to_dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    W, R = WINDOW, SHARE
+    q, k, v, kc, vc = synth.qkv(W["seed"], W["B"], W["H"], W["S"], W["S"], W["D"], ctx=W["ctx"])
+    q, k, v, kc, vc = (to_dev(x) for x in (q, k, v, kc, vc))
+    rq, rk, rv = (to_dev(x) for x in synth.qkv(R["seed"], R["B"], R["H"], R["S"], R["S"], R["D"]))
+    scale = synth.default_scale(W["D"])
+    B, H, S, D = W["B"], W["H"], W["S"], W["D"]
+    o_self = torch.empty((B, S, H, D), dtype=torch.bfloat16, device=dev)
+    l_self = torch.empty((B, H, S), dtype=torch.float32, device=dev)
+    o_cross = torch.empty_like(o_self)
+    l_cross = torch.empty_like(l_self)
+    nch = R["chunks"]
+    csz = R["S"] // nch
+    bounds = [i * csz for i in range(nch)] + [R["S"]]
+    o_parts = [torch.empty((R["B"], R["S"], R["H"], R["D"]), dtype=torch.float32, device=dev) for _ in range(nch)]
+    l_parts = [torch.empty((R["B"], R["H"], R["S"]), dtype=torch.float32, device=dev) for _ in range(nch)]
+    o_share = torch.empty((R["B"], R["S"], R["H"], R["D"]), dtype=torch.bfloat16, device=dev)
+    l_share = torch.empty((R["B"], R["H"], R["S"]), dtype=torch.float32, device=dev)
+
+    comps = ["self", "cross", "share"] if args.only is None else [args.only]
+    flops = {
+        "self": attn_flops(B, H, S, S, D),
+        "cross": attn_flops(B, H, S, W["ctx"], D),
+        "share": attn_flops(R["B"], R["H"], R["S"], R["S"], R["D"]),
+    }
+    stream = torch.cuda.current_stream(dev)
+    ev = {c: [] for c in comps}
+
+    def step(record):
+        for c in comps:
+            if record:
+                e0 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+            if c == "self":
+                api.attn_fwd(q, k, v, scale=scale, out=o_self, lse_out=l_self)
+            elif c == "cross":
+                api.cross_attn_fwd(q, kc, vc, scale=scale, out=o_cross, lse_out=l_cross)
+            else:
+                for i in range(nch):
+                    a, b = bounds[i], bounds[i + 1]
+                    api.attn_partial_fwd(rq, rk[:, a:b], rv[:, a:b], scale=scale, out=o_parts[i], lse_out=l_parts[i])
+                api.lse_merge(o_parts, l_parts, out=o_share, lse_out=l_share)
+            if record:
+                e1 = torch.cuda.Event(enable_timing=True)
+                e1.record(stream)
+                ev[c].append((e0, e1))
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done ({args.warmup} steps), timing {args.steps} steps of {comps}", file=sys.stderr,
+          flush=True)
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for _ in range(args.steps):
+        step(True)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_per_step = total_ms / args.steps
+    step_flops = sum(flops[c] for c in comps)
+    value = step_flops / (ms_per_step * 1e-3) / 1e12
+
+    components = {}
+    for c in comps:
+        times = sorted(e0.elapsed_time(e1) for e0, e1 in ev[c])
+        avg = sum(times) / len(times)
+        components[c] = {"ms_avg": avg, "ms_median": times[len(times) // 2], "ms_min": times[0],
+                         "gflop": flops[c] / 1e9, "tflops": flops[c] / (avg * 1e-3) / 1e12}
+    if "share" in comps:
+        # merge traffic: reads 4 x (fp32 O + LSE), writes bf16 O + LSE
+        rows = R["B"] * R["S"] * R["H"]
+        components["share"]["merge_bytes"] = nch * rows * (R["D"] * 4 + 4) + rows * (R["D"] * 2 + 4)
+
+    dom = "self" if "self" in comps else comps[0]
+    achieved = components[dom]["tflops"]
+    roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None, "kernel": f"attention ({dom})"}
+
+    line = {
+        "metric": "attention TFLOP/s (bf16) at S=10920,H=12,d=128; % of MFMA bf16 peak",
+        "value": value,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "pct_of_peak": 100.0 * value / PEAK_BF16_TFLOPS,
+        "config": {
+            "workload": "25-frame window attention: self-attn S=10920 (7x30x52) H=12 d=128 bf16 + cross-attn "
+                        "to 512 ctx tokens + one rank share (H=5, 4 key chunks of 2730, partials + LSE merge)"
+            if args.only is None else f"component '{args.only}' only",
+            "components": comps, "B": B, "H": H, "S": S, "d": D, "ctx": W["ctx"],
+            "share": {"H": R["H"], "Sq": R["S"], "chunks": nch, "chunk": csz},
+            "inputs": "i.i.d. N(0,1) bf16, seeds 3 (window) and 4 (share)",
+            "parallelism": "single GPU",
+        },
+        "components": components,
+        "roofline": roofline,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline and args.only is None:
+        print("[bench] timing the oracle on the host cores", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,148 @@
+/*
+ * regenvc_attn.h -- C ABI of the gfx950 (MI355X) window-attention library.
+ *
+ * The operations are the per-GPU compute of the decoder's sequence-parallel
+ * attention (paper Sec. 3.5, "Multi-GPU unified sequence parallelism"):
+ *   - Ulysses hands every GPU the whole token sequence for a subset of heads
+ *     and asks for exact attention over it                -> regenvc_attn_fwd
+ *   - Ring streams key/value blocks between GPUs and combines them
+ *     online-softmax style: one partial result per key/value chunk, then a
+ *     log-sum-exp merge that is exact up to reduction order
+ *                            -> regenvc_attn_partial_fwd + regenvc_lse_merge
+ *   - the conditioning path (Sec. 3.9, "Hybrid CPU-GPU deployment") streams
+ *     precomputed text/image key/value tensors to the GPU, which the video
+ *     tokens cross-attend to                         -> regenvc_cross_attn_fwd
+ *
+ * Definition (per batch b, head h, query row i; scale = softmax_scale):
+ *     s_j = scale * <Q[b,i,h,:], K[b,j,h,:]>,  j = 0..Skv-1
+ *     O[b,i,h,:] = sum_j softmax(s)_j * V[b,j,h,:]
+ *     LSE[b,h,i] = log sum_j exp(s_j)                      (natural log)
+ * Attention is non-causal and unmasked: every query sees every key of the
+ * window.
+ *
+ * Conventions common to every entry point
+ *   - Every data pointer is DEVICE memory owned by the caller; the library
+ *     never frees, keeps or synchronizes on it.
+ *   - Q/K/V/O are logical [B, S, H, D] with element strides for b, s and h
+ *     (regenvc_tensor); the D axis is contiguous.  Token-major [B,S,H,D]
+ *     and head-major [B,H,S,D] are both expressible.  Inputs are bf16.
+ *   - LSE buffers are float32, contiguous [B, H, Sq].
+ *   - Arguments are validated synchronously, before any HIP call.  On any
+ *     error the call returns a non-OK status, enqueues nothing and leaves
+ *     every output untouched; regenvc_last_error() then describes the
+ *     problem (thread-local text).
+ *   - On success the work is enqueued asynchronously on `stream`
+ *     (a hipStream_t; NULL = the legacy default stream).  Device faults
+ *     surface at the caller's next synchronization.
+ *   - Outputs must not overlap any input or each other.
+ *   - B, H or Sq equal to 0 is an empty problem: OK, nothing enqueued.
+ *   - Only D in {64, 128} is implemented; only gfx950 devices are accepted.
+ *   - All entry points are reentrant; concurrent calls on different streams
+ *     are independent.
+ *   - The same launch configuration gives bit-identical results run to run.
+ */
+#ifndef REGENVC_ATTN_H
+#define REGENVC_ATTN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    REGENVC_OK = 0,
+    /* NULL pointer, negative size, Skv < 1, non-finite or negative scale,
+       num_parts out of range, overlapping output and input */
+    REGENVC_ERR_INVALID_ARG = 1,
+    /* D not in {64,128}; pointer not 16-byte aligned; a stride not a
+       multiple of 8 elements; a size whose element offsets overflow int64;
+       the current device is not gfx950 */
+    REGENVC_ERR_UNSUPPORTED = 2,
+    /* a HIP runtime call failed (device query or kernel launch) */
+    REGENVC_ERR_HIP = 3
+} regenvc_status;
+
+typedef enum { REGENVC_BF16 = 0, REGENVC_F32 = 1 } regenvc_dtype;
+
+/* A logical [B, S, H, D] tensor: base pointer plus element strides of the
+   b, s and h axes (the d axis has stride 1).  Strides may be any value that
+   is a multiple of 8 elements, including 0 (broadcast). */
+typedef struct {
+    void *ptr;
+    int64_t stride_b;
+    int64_t stride_s;
+    int64_t stride_h;
+} regenvc_tensor;
+
+#define REGENVC_MAX_PARTS 16
+
+/* Exact self-attention over the full key sequence for H heads
+   (Sec. 3.5, Ulysses: "exact attention over the full sequence for a subset
+   of heads").
+     q: bf16 [B,Sq,H,D]; k, v: bf16 [B,Skv,H,D]
+     o: [B,Sq,H,D] in o_dtype (bf16, round-to-nearest-even, or f32)
+     lse: f32 [B,H,Sq] or NULL to skip it
+     softmax_scale: finite, >= 0 (the usual value is 1/sqrt(D))
+   Skv must be >= 1. */
+regenvc_status regenvc_attn_fwd(const regenvc_tensor *q, const regenvc_tensor *k,
+                                const regenvc_tensor *v, const regenvc_tensor *o,
+                                regenvc_dtype o_dtype, float *lse,
+                                int32_t B, int32_t H, int32_t Sq, int32_t Skv,
+                                int32_t D, float softmax_scale, void *stream);
+
+/* Partial attention of every query over ONE key/value chunk (Sec. 3.5,
+   Ring: key/value blocks are streamed and combined online-softmax style).
+   The chunk is a plain view: k_chunk/v_chunk point at the chunk's first
+   token with the full tensor's strides.
+     o_part: f32 [B,Sq,H,D], normalized over the chunk's keys
+     lse_part: f32 [B,H,Sq], required (the merge needs it)
+   Skv_chunk == 0 is allowed and writes the merge identity: o_part = 0,
+   lse_part = -inf. */
+regenvc_status regenvc_attn_partial_fwd(const regenvc_tensor *q,
+                                        const regenvc_tensor *k_chunk,
+                                        const regenvc_tensor *v_chunk,
+                                        const regenvc_tensor *o_part, float *lse_part,
+                                        int32_t B, int32_t H, int32_t Sq,
+                                        int32_t Skv_chunk, int32_t D,
+                                        float softmax_scale, void *stream);
+
+/* Log-sum-exp merge of num_parts partial results over disjoint key chunks
+   into the result over their union (Sec. 3.5: the sharded computation equals
+   single-device attention up to reduction order):
+     m = max_c L_c;  L = m + log sum_c exp(L_c - m);  O = sum_c exp(L_c - L) O_c
+   A part with L_c = -inf has weight 0; if every part is -inf the row is
+   O = 0, L = -inf.
+     o_parts, lse_parts: HOST arrays of num_parts DEVICE pointers;
+       o_parts[c]: f32 [B,Sq,H,D] contiguous; lse_parts[c]: f32 [B,H,Sq]
+     1 <= num_parts <= REGENVC_MAX_PARTS
+     o: [B,Sq,H,D] in o_dtype; lse: f32 [B,H,Sq] or NULL.
+   The result does not depend on the order of the parts beyond rounding. */
+regenvc_status regenvc_lse_merge(const float *const *o_parts,
+                                 const float *const *lse_parts, int32_t num_parts,
+                                 const regenvc_tensor *o, regenvc_dtype o_dtype,
+                                 float *lse, int32_t B, int32_t H, int32_t Sq,
+                                 int32_t D, void *stream);
+
+/* Cross-attention of the video tokens to Sctx conditioning tokens whose
+   key/value tensors were precomputed off-GPU and uploaded (Sec. 3.9).
+   Same definition, layouts and rules as regenvc_attn_fwd with Skv = Sctx. */
+regenvc_status regenvc_cross_attn_fwd(const regenvc_tensor *q,
+                                      const regenvc_tensor *k_ctx,
+                                      const regenvc_tensor *v_ctx,
+                                      const regenvc_tensor *o, regenvc_dtype o_dtype,
+                                      float *lse, int32_t B, int32_t H, int32_t Sq,
+                                      int32_t Sctx, int32_t D, float softmax_scale,
+                                      void *stream);
+
+/* Static text for a status code. */
+const char *regenvc_status_str(regenvc_status status);
+
+/* Detail of the most recent non-OK return on the calling thread ("" if none). */
+const char *regenvc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* REGENVC_ATTN_H */

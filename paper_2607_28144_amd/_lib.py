@@ -1,0 +1,69 @@
+"""ctypes declarations of the C ABI in include/regenvc_attn.h."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libregenvc_attn.so")
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP = 0, 1, 2, 3
+BF16, F32 = 0, 1
+MAX_PARTS = 16
+
+
+class Tensor(ctypes.Structure):
+    """regenvc_tensor: base pointer + element strides of the b, s, h axes."""
+    _fields_ = [("ptr", ctypes.c_void_p), ("stride_b", ctypes.c_int64),
+                ("stride_s", ctypes.c_int64), ("stride_h", ctypes.c_int64)]
+
+
+class RegenvcError(RuntimeError):
+    def __init__(self, status: int, fn: str, detail: str):
+        self.status = status
+        super().__init__(f"{fn} failed with status {status}: {detail}")
+
+
+_PT = ctypes.POINTER(Tensor)
+_i32 = ctypes.c_int32
+_FP = ctypes.POINTER(ctypes.c_float)
+_SIGNATURES = {
+    "regenvc_attn_fwd": [_PT, _PT, _PT, _PT, ctypes.c_int, ctypes.c_void_p,
+                         _i32, _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_void_p],
+    "regenvc_attn_partial_fwd": [_PT, _PT, _PT, _PT, ctypes.c_void_p,
+                                 _i32, _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_void_p],
+    "regenvc_lse_merge": [ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(ctypes.c_void_p), _i32,
+                          _PT, ctypes.c_int, ctypes.c_void_p, _i32, _i32, _i32, _i32, ctypes.c_void_p],
+    "regenvc_cross_attn_fwd": [_PT, _PT, _PT, _PT, ctypes.c_int, ctypes.c_void_p,
+                               _i32, _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_void_p],
+}
+
+_lib = None
+
+
+def load(path: str | None = None) -> ctypes.CDLL:
+    """Loads the built library (once).  Fails loudly if it has not been built:
+    there is no fallback implementation."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise ImportError(f"{p} is missing; build it with `python -m paper_2607_28144_amd.build`")
+    lib = ctypes.CDLL(p)
+    for name, argtypes in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.argtypes = argtypes
+        fn.restype = ctypes.c_int
+    lib.regenvc_status_str.argtypes = [ctypes.c_int]
+    lib.regenvc_status_str.restype = ctypes.c_char_p
+    lib.regenvc_last_error.argtypes = []
+    lib.regenvc_last_error.restype = ctypes.c_char_p
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def check(status: int, fn: str) -> None:
+    if status != OK:
+        detail = load().regenvc_last_error().decode(errors="replace")
+        raise RegenvcError(status, fn, detail)

@@ -1,0 +1,130 @@
+"""Thin torch-facing binding of the C ABI (argument marshalling only).
+
+Every step of the computation runs in the HIP kernels of libregenvc_attn.so;
+torch supplies device memory and the current stream.  Tensors are logical
+[B, S, H, D] views (any b/s/h strides that are multiples of 8 elements, d
+contiguous); LSE tensors are float32 [B, H, Sq].
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+from typing import Optional, Sequence, Tuple
+
+import torch
+
+from . import _lib
+from ._lib import RegenvcError  # noqa: F401  (re-export)
+
+_DT = {torch.bfloat16: _lib.BF16, torch.float32: _lib.F32}
+
+
+def _desc(t: torch.Tensor, name: str, dtype: torch.dtype) -> _lib.Tensor:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor, got {t.device}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != 4:
+        raise ValueError(f"{name} must be [B, S, H, D], got shape {tuple(t.shape)}")
+    if t.numel() > 0 and t.shape[3] > 1 and t.stride(3) != 1:
+        raise ValueError(f"{name}: the head-dim axis must be contiguous")
+    return _lib.Tensor(t.data_ptr(), t.stride(0), t.stride(1), t.stride(2))
+
+
+def _stream(device: torch.device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _fptr(t: Optional[torch.Tensor], name: str, shape) -> Optional[int]:
+    if t is None:
+        return None
+    if t.dtype != torch.float32 or not t.is_contiguous() or tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must be a contiguous float32 tensor of shape {tuple(shape)}")
+    return t.data_ptr()
+
+
+def _scale(scale: Optional[float], D: int) -> float:
+    return float(torch.tensor(1.0 / math.sqrt(D), dtype=torch.float32)) if scale is None else float(scale)
+
+
+def _attn(fn_name: str, q, k, v, scale, out_dtype, out, want_lse, lse_out):
+    B, Sq, H, D = q.shape
+    Skv = k.shape[1]
+    if tuple(k.shape) != (B, Skv, H, D) or tuple(v.shape) != (B, Skv, H, D):
+        raise ValueError(f"k/v shapes {tuple(k.shape)}, {tuple(v.shape)} do not match q {tuple(q.shape)}")
+    if out is None:
+        out = torch.empty((B, Sq, H, D), dtype=out_dtype, device=q.device)
+    if lse_out is None and want_lse:
+        lse_out = torch.empty((B, H, Sq), dtype=torch.float32, device=q.device)
+    qd, kd, vd = _desc(q, "q", torch.bfloat16), _desc(k, "k", torch.bfloat16), _desc(v, "v", torch.bfloat16)
+    od = _desc(out, "out", out_dtype)
+    lp = _fptr(lse_out, "lse", (B, H, Sq))
+    lib = _lib.load()
+    with torch.cuda.device(q.device):
+        if fn_name == "regenvc_attn_partial_fwd":
+            st = lib.regenvc_attn_partial_fwd(ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), ctypes.byref(od),
+                                              lp, B, H, Sq, Skv, D, _scale(scale, D), _stream(q.device))
+        else:
+            st = getattr(lib, fn_name)(ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), ctypes.byref(od),
+                                       _DT[out_dtype], lp, B, H, Sq, Skv, D, _scale(scale, D), _stream(q.device))
+    _lib.check(st, fn_name)
+    return out, lse_out
+
+
+def attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, scale: Optional[float] = None,
+             out_dtype: torch.dtype = torch.bfloat16, out: Optional[torch.Tensor] = None,
+             return_lse: bool = True, lse_out: Optional[torch.Tensor] = None
+             ) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """Exact self-attention over all keys (regenvc_attn_fwd).  Returns (O, LSE or None)."""
+    return _attn("regenvc_attn_fwd", q, k, v, scale, out_dtype, out, return_lse, lse_out)
+
+
+def attn_partial_fwd(q: torch.Tensor, k_chunk: torch.Tensor, v_chunk: torch.Tensor,
+                     scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
+                     lse_out: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Partial attention over one key/value chunk (regenvc_attn_partial_fwd):
+    float32 O normalized over the chunk, and its LSE."""
+    return _attn("regenvc_attn_partial_fwd", q, k_chunk, v_chunk, scale, torch.float32, out, True, lse_out)
+
+
+def cross_attn_fwd(q: torch.Tensor, k_ctx: torch.Tensor, v_ctx: torch.Tensor, scale: Optional[float] = None,
+                   out_dtype: torch.dtype = torch.bfloat16, out: Optional[torch.Tensor] = None,
+                   return_lse: bool = True, lse_out: Optional[torch.Tensor] = None
+                   ) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """Cross-attention to conditioning tokens (regenvc_cross_attn_fwd)."""
+    return _attn("regenvc_cross_attn_fwd", q, k_ctx, v_ctx, scale, out_dtype, out, return_lse, lse_out)
+
+
+def lse_merge(o_parts: Sequence[torch.Tensor], lse_parts: Sequence[torch.Tensor],
+              out_dtype: torch.dtype = torch.bfloat16, out: Optional[torch.Tensor] = None,
+              return_lse: bool = True, lse_out: Optional[torch.Tensor] = None
+              ) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """Log-sum-exp merge of chunk partials (regenvc_lse_merge)."""
+    n = len(o_parts)
+    if n != len(lse_parts) or n < 1:
+        raise ValueError("need the same, non-zero number of o_parts and lse_parts")
+    B, Sq, H, D = o_parts[0].shape
+    for t in o_parts:
+        if tuple(t.shape) != (B, Sq, H, D) or t.dtype != torch.float32 or not t.is_contiguous() \
+                or t.device != o_parts[0].device:
+            raise ValueError("o_parts must be contiguous float32 [B, Sq, H, D] tensors on one device")
+    for t in lse_parts:
+        if tuple(t.shape) != (B, H, Sq) or t.dtype != torch.float32 or not t.is_contiguous() \
+                or t.device != o_parts[0].device:
+            raise ValueError("lse_parts must be contiguous float32 [B, H, Sq] tensors on one device")
+    dev = o_parts[0].device
+    if out is None:
+        out = torch.empty((B, Sq, H, D), dtype=out_dtype, device=dev)
+    if lse_out is None and return_lse:
+        lse_out = torch.empty((B, H, Sq), dtype=torch.float32, device=dev)
+    od = _desc(out, "out", out_dtype)
+    optrs = (ctypes.c_void_p * n)(*[t.data_ptr() for t in o_parts])
+    lptrs = (ctypes.c_void_p * n)(*[t.data_ptr() for t in lse_parts])
+    lp = _fptr(lse_out, "lse", (B, H, Sq))
+    lib = _lib.load()
+    with torch.cuda.device(dev):
+        st = lib.regenvc_lse_merge(optrs, lptrs, n, ctypes.byref(od), _DT[out_dtype], lp, B, H, Sq, D, _stream(dev))
+    _lib.check(st, "regenvc_lse_merge")
+    return out, lse_out

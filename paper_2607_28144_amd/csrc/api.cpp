@@ -1,0 +1,342 @@
+// C ABI of the window-attention library: synchronous argument validation
+// (before any HIP call), device check, and kernel launch on the caller's
+// stream.  Declarations and the contract live in include/regenvc_attn.h.
+#include "regenvc_attn.h"
+
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "attn_kernels.hpp"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+regenvc_status fail(regenvc_status st, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+// Byte range [lo, hi) that a logical [B,S,H,D] view can touch.
+struct Extent {
+    uintptr_t lo, hi;
+};
+
+bool mul_ok(int64_t a, int64_t b, int64_t *out)
+{
+    return !__builtin_mul_overflow(a, b, out);
+}
+
+// Checks one tensor view; on success fills its byte extent.
+regenvc_status check_view(const char *name, const regenvc_tensor *t, int64_t B, int64_t S, int64_t H, int64_t D,
+                          size_t elem, Extent *ext)
+{
+    if (t == nullptr) return fail(REGENVC_ERR_INVALID_ARG, "%s: descriptor is NULL", name);
+    if (t->ptr == nullptr) return fail(REGENVC_ERR_INVALID_ARG, "%s: data pointer is NULL", name);
+    if (reinterpret_cast<uintptr_t>(t->ptr) % 16 != 0)
+        return fail(REGENVC_ERR_UNSUPPORTED, "%s: data pointer is not 16-byte aligned", name);
+    const int64_t strides[3] = {t->stride_b, t->stride_s, t->stride_h};
+    const int64_t sizes[3] = {B, S, H};
+    const char *axis[3] = {"b", "s", "h"};
+    int64_t lo = 0, hi = D;  // element offsets relative to ptr
+    for (int i = 0; i < 3; ++i) {
+        if (strides[i] % 8 != 0)
+            return fail(REGENVC_ERR_UNSUPPORTED, "%s: stride_%s=%lld is not a multiple of 8 elements", name, axis[i],
+                        (long long)strides[i]);
+        int64_t span;
+        if (!mul_ok(strides[i], sizes[i] - 1, &span))
+            return fail(REGENVC_ERR_UNSUPPORTED, "%s: offsets overflow int64", name);
+        if (span < 0) {
+            if (__builtin_add_overflow(lo, span, &lo))
+                return fail(REGENVC_ERR_UNSUPPORTED, "%s: offsets overflow int64", name);
+        } else if (__builtin_add_overflow(hi, span, &hi)) {
+            return fail(REGENVC_ERR_UNSUPPORTED, "%s: offsets overflow int64", name);
+        }
+    }
+    int64_t blo, bhi;
+    if (!mul_ok(lo, (int64_t)elem, &blo) || !mul_ok(hi, (int64_t)elem, &bhi))
+        return fail(REGENVC_ERR_UNSUPPORTED, "%s: byte offsets overflow int64", name);
+    const uintptr_t base = reinterpret_cast<uintptr_t>(t->ptr);
+    ext->lo = base + (intptr_t)blo;
+    ext->hi = base + (intptr_t)bhi;
+    return REGENVC_OK;
+}
+
+Extent flat_extent(const void *p, int64_t n_elems, size_t elem)
+{
+    const uintptr_t base = reinterpret_cast<uintptr_t>(p);
+    return Extent{base, base + (uintptr_t)(n_elems * (int64_t)elem)};
+}
+
+bool overlap(const Extent &a, const Extent &b)
+{
+    return a.lo < b.hi && b.lo < a.hi;
+}
+
+// An output view must not map two logical elements to one address: sorted
+// by |stride|, every axis of size > 1 must step past the whole span of the
+// axes inside it (d is the innermost axis, stride 1, size D).
+bool view_is_injective(const regenvc_tensor *t, int64_t B, int64_t S, int64_t H, int64_t D)
+{
+    int64_t st[3] = {t->stride_b, t->stride_s, t->stride_h};
+    int64_t sz[3] = {B, S, H};
+    for (int i = 0; i < 3; ++i) st[i] = st[i] < 0 ? -st[i] : st[i];
+    for (int i = 0; i < 3; ++i)  // tiny insertion sort by stride
+        for (int j = i + 1; j < 3; ++j)
+            if (st[j] < st[i]) {
+                int64_t a = st[i], b = sz[i];
+                st[i] = st[j], sz[i] = sz[j];
+                st[j] = a, sz[j] = b;
+            }
+    int64_t span = D;  // elements covered by the axes inside the current one
+    for (int i = 0; i < 3; ++i) {
+        if (sz[i] <= 1) continue;
+        if (st[i] < span) return false;
+        span = st[i] * sz[i];
+    }
+    return true;
+}
+
+regenvc_status check_sizes(int32_t B, int32_t H, int32_t Sq, int32_t D)
+{
+    if (B < 0 || H < 0 || Sq < 0)
+        return fail(REGENVC_ERR_INVALID_ARG, "negative size (B=%d H=%d Sq=%d)", B, H, Sq);
+    if (D != 64 && D != 128) return fail(REGENVC_ERR_UNSUPPORTED, "head dim D=%d (only 64 and 128)", D);
+    return REGENVC_OK;
+}
+
+regenvc_status check_scale(float s)
+{
+    if (!std::isfinite(s)) return fail(REGENVC_ERR_INVALID_ARG, "softmax_scale is not finite");
+    if (s < 0.f) return fail(REGENVC_ERR_INVALID_ARG, "softmax_scale is negative");
+    return REGENVC_OK;
+}
+
+// Device must be gfx950.  Cached per device ordinal.
+std::atomic<int> g_arch_state[64];  // 0 unknown, 1 ok, 2 wrong arch
+
+regenvc_status check_device()
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(REGENVC_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    int st = (dev >= 0 && dev < 64) ? g_arch_state[dev].load() : 0;
+    if (st == 0) {
+        hipDeviceProp_t prop;
+        e = hipGetDeviceProperties(&prop, dev);
+        if (e != hipSuccess) return fail(REGENVC_ERR_HIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
+        st = (std::strncmp(prop.gcnArchName, "gfx950", 6) == 0) ? 1 : 2;
+        if (dev >= 0 && dev < 64) g_arch_state[dev].store(st);
+        if (st == 2)
+            return fail(REGENVC_ERR_UNSUPPORTED, "device %d is %s; this library is built for gfx950 only", dev,
+                        prop.gcnArchName);
+    }
+    if (st == 2) return fail(REGENVC_ERR_UNSUPPORTED, "device %d is not gfx950", dev);
+    return REGENVC_OK;
+}
+
+regenvc_status launched(hipError_t e, const char *what)
+{
+    if (e != hipSuccess) return fail(REGENVC_ERR_HIP, "%s launch: %s", what, hipGetErrorString(e));
+    g_last_error[0] = '\0';
+    return REGENVC_OK;
+}
+
+regenvc_status attn_common(const char *fn, const regenvc_tensor *q, const regenvc_tensor *k,
+                           const regenvc_tensor *v, const regenvc_tensor *o, regenvc_dtype o_dtype, float *lse,
+                           bool lse_required, int32_t B, int32_t H, int32_t Sq, int32_t Skv, int32_t D, float scale,
+                           void *stream, bool allow_empty_keys)
+{
+    regenvc_status st = check_sizes(B, H, Sq, D);
+    if (st != REGENVC_OK) return st;
+    if (Skv < 0 || (Skv == 0 && !allow_empty_keys))
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: key count %d must be >= 1", fn, Skv);
+    if (o_dtype != REGENVC_BF16 && o_dtype != REGENVC_F32)
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: unknown output dtype %d", fn, (int)o_dtype);
+    if ((st = check_scale(scale)) != REGENVC_OK) return st;
+    if (lse_required && lse == nullptr) return fail(REGENVC_ERR_INVALID_ARG, "%s: lse output is required", fn);
+    if (lse != nullptr && reinterpret_cast<uintptr_t>(lse) % 4 != 0)
+        return fail(REGENVC_ERR_UNSUPPORTED, "%s: lse pointer is not 4-byte aligned", fn);
+    if (B == 0 || H == 0 || Sq == 0) {
+        // empty problem: nothing to read or write, but descriptors must still be present
+        if (!q || !k || !v || !o) return fail(REGENVC_ERR_INVALID_ARG, "%s: descriptor is NULL", fn);
+        g_last_error[0] = '\0';
+        return REGENVC_OK;
+    }
+    const int64_t Skv_view = Skv > 0 ? Skv : 1;
+    Extent eq, ek, ev, eo;
+    if ((st = check_view("q", q, B, Sq, H, D, 2, &eq)) != REGENVC_OK) return st;
+    if (Skv > 0) {
+        if ((st = check_view("k", k, B, Skv_view, H, D, 2, &ek)) != REGENVC_OK) return st;
+        if ((st = check_view("v", v, B, Skv_view, H, D, 2, &ev)) != REGENVC_OK) return st;
+    } else if (!k || !v) {
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: descriptor is NULL", fn);
+    }
+    const size_t oel = o_dtype == REGENVC_F32 ? 4 : 2;
+    if ((st = check_view("o", o, B, Sq, H, D, oel, &eo)) != REGENVC_OK) return st;
+    if (!view_is_injective(o, B, Sq, H, D))
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: output o has overlapping rows (strides)", fn);
+    if (overlap(eo, eq) || (Skv > 0 && (overlap(eo, ek) || overlap(eo, ev))))
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: output o overlaps an input", fn);
+    if (lse != nullptr) {
+        const Extent el = flat_extent(lse, (int64_t)B * H * Sq, 4);
+        if (overlap(el, eq) || overlap(el, eo) || (Skv > 0 && (overlap(el, ek) || overlap(el, ev))))
+            return fail(REGENVC_ERR_INVALID_ARG, "%s: lse overlaps another tensor", fn);
+    }
+    if ((st = check_device()) != REGENVC_OK) return st;
+
+    if (Skv == 0) {  // empty chunk: the merge identity
+        regenvc::FillArgs f{};
+        f.o = static_cast<float *>(o->ptr);
+        f.lse = lse;
+        f.o_sb = o->stride_b;
+        f.o_ss = o->stride_s;
+        f.o_sh = o->stride_h;
+        f.B = B;
+        f.H = H;
+        f.Sq = Sq;
+        f.D = D;
+        return launched(regenvc::launch_empty_partial(f, static_cast<hipStream_t>(stream)), fn);
+    }
+    regenvc::AttnArgs a{};
+    a.q = q->ptr;
+    a.k = k->ptr;
+    a.v = v->ptr;
+    a.o = o->ptr;
+    a.lse = lse;
+    a.q_sb = q->stride_b, a.q_ss = q->stride_s, a.q_sh = q->stride_h;
+    a.k_sb = k->stride_b, a.k_ss = k->stride_s, a.k_sh = k->stride_h;
+    a.v_sb = v->stride_b, a.v_ss = v->stride_s, a.v_sh = v->stride_h;
+    a.o_sb = o->stride_b, a.o_ss = o->stride_s, a.o_sh = o->stride_h;
+    a.B = B;
+    a.H = H;
+    a.Sq = Sq;
+    a.Skv = Skv;
+    a.D = D;
+    a.o_f32 = o_dtype == REGENVC_F32;
+    a.scale = scale;
+    return launched(regenvc::launch_attn(a, static_cast<hipStream_t>(stream)), fn);
+}
+
+}  // namespace
+
+extern "C" {
+
+regenvc_status regenvc_attn_fwd(const regenvc_tensor *q, const regenvc_tensor *k, const regenvc_tensor *v,
+                                const regenvc_tensor *o, regenvc_dtype o_dtype, float *lse, int32_t B, int32_t H,
+                                int32_t Sq, int32_t Skv, int32_t D, float softmax_scale, void *stream)
+{
+    return attn_common("regenvc_attn_fwd", q, k, v, o, o_dtype, lse, false, B, H, Sq, Skv, D, softmax_scale, stream,
+                       false);
+}
+
+regenvc_status regenvc_attn_partial_fwd(const regenvc_tensor *q, const regenvc_tensor *k_chunk,
+                                        const regenvc_tensor *v_chunk, const regenvc_tensor *o_part,
+                                        float *lse_part, int32_t B, int32_t H, int32_t Sq, int32_t Skv_chunk,
+                                        int32_t D, float softmax_scale, void *stream)
+{
+    return attn_common("regenvc_attn_partial_fwd", q, k_chunk, v_chunk, o_part, REGENVC_F32, lse_part, true, B, H, Sq,
+                       Skv_chunk, D, softmax_scale, stream, true);
+}
+
+regenvc_status regenvc_cross_attn_fwd(const regenvc_tensor *q, const regenvc_tensor *k_ctx,
+                                      const regenvc_tensor *v_ctx, const regenvc_tensor *o, regenvc_dtype o_dtype,
+                                      float *lse, int32_t B, int32_t H, int32_t Sq, int32_t Sctx, int32_t D,
+                                      float softmax_scale, void *stream)
+{
+    return attn_common("regenvc_cross_attn_fwd", q, k_ctx, v_ctx, o, o_dtype, lse, false, B, H, Sq, Sctx, D,
+                       softmax_scale, stream, false);
+}
+
+regenvc_status regenvc_lse_merge(const float *const *o_parts, const float *const *lse_parts, int32_t num_parts,
+                                 const regenvc_tensor *o, regenvc_dtype o_dtype, float *lse, int32_t B, int32_t H,
+                                 int32_t Sq, int32_t D, void *stream)
+{
+    regenvc_status st = check_sizes(B, H, Sq, D);
+    if (st != REGENVC_OK) return st;
+    if (num_parts < 1 || num_parts > REGENVC_MAX_PARTS)
+        return fail(REGENVC_ERR_INVALID_ARG, "regenvc_lse_merge: num_parts=%d not in [1, %d]", num_parts,
+                    REGENVC_MAX_PARTS);
+    if (o_parts == nullptr || lse_parts == nullptr)
+        return fail(REGENVC_ERR_INVALID_ARG, "regenvc_lse_merge: part arrays are NULL");
+    if (o_dtype != REGENVC_BF16 && o_dtype != REGENVC_F32)
+        return fail(REGENVC_ERR_INVALID_ARG, "regenvc_lse_merge: unknown output dtype %d", (int)o_dtype);
+    if (o == nullptr) return fail(REGENVC_ERR_INVALID_ARG, "regenvc_lse_merge: descriptor is NULL");
+    for (int c = 0; c < num_parts; ++c) {
+        if (o_parts[c] == nullptr || lse_parts[c] == nullptr)
+            return fail(REGENVC_ERR_INVALID_ARG, "regenvc_lse_merge: part %d pointer is NULL", c);
+        if (reinterpret_cast<uintptr_t>(o_parts[c]) % 16 != 0)
+            return fail(REGENVC_ERR_UNSUPPORTED, "regenvc_lse_merge: o_parts[%d] is not 16-byte aligned", c);
+        if (reinterpret_cast<uintptr_t>(lse_parts[c]) % 4 != 0)
+            return fail(REGENVC_ERR_UNSUPPORTED, "regenvc_lse_merge: lse_parts[%d] is not 4-byte aligned", c);
+    }
+    if (lse != nullptr && reinterpret_cast<uintptr_t>(lse) % 4 != 0)
+        return fail(REGENVC_ERR_UNSUPPORTED, "regenvc_lse_merge: lse pointer is not 4-byte aligned");
+    if (B == 0 || H == 0 || Sq == 0) {
+        g_last_error[0] = '\0';
+        return REGENVC_OK;
+    }
+    Extent eo;
+    if ((st = check_view("o", o, B, Sq, H, D, o_dtype == REGENVC_F32 ? 4 : 2, &eo)) != REGENVC_OK) return st;
+    if (!view_is_injective(o, B, Sq, H, D))
+        return fail(REGENVC_ERR_INVALID_ARG, "regenvc_lse_merge: output o has overlapping rows (strides)");
+    const int64_t rows = (int64_t)B * Sq * H;
+    Extent el{0, 0};
+    if (lse != nullptr) el = flat_extent(lse, (int64_t)B * H * Sq, 4);
+    for (int c = 0; c < num_parts; ++c) {
+        const Extent ep = flat_extent(o_parts[c], rows * D, 4);
+        const Extent elp = flat_extent(lse_parts[c], rows, 4);
+        if (overlap(eo, ep) || overlap(eo, elp))
+            return fail(REGENVC_ERR_INVALID_ARG, "regenvc_lse_merge: output o overlaps part %d", c);
+        if (lse != nullptr && (overlap(el, ep) || overlap(el, elp)))
+            return fail(REGENVC_ERR_INVALID_ARG, "regenvc_lse_merge: output lse overlaps part %d", c);
+    }
+    if (lse != nullptr && overlap(el, eo))
+        return fail(REGENVC_ERR_INVALID_ARG, "regenvc_lse_merge: lse overlaps o");
+    if ((st = check_device()) != REGENVC_OK) return st;
+
+    regenvc::MergeArgs m{};
+    for (int c = 0; c < num_parts; ++c) {
+        m.o_parts[c] = o_parts[c];
+        m.lse_parts[c] = lse_parts[c];
+    }
+    m.num_parts = num_parts;
+    m.o = o->ptr;
+    m.lse = lse;
+    m.o_sb = o->stride_b;
+    m.o_ss = o->stride_s;
+    m.o_sh = o->stride_h;
+    m.B = B;
+    m.H = H;
+    m.Sq = Sq;
+    m.D = D;
+    m.o_f32 = o_dtype == REGENVC_F32;
+    return launched(regenvc::launch_merge(m, static_cast<hipStream_t>(stream)), "regenvc_lse_merge");
+}
+
+const char *regenvc_status_str(regenvc_status status)
+{
+    switch (status) {
+    case REGENVC_OK: return "ok";
+    case REGENVC_ERR_INVALID_ARG: return "invalid argument";
+    case REGENVC_ERR_UNSUPPORTED: return "unsupported";
+    case REGENVC_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+const char *regenvc_last_error(void)
+{
+    return g_last_error;
+}
+
+}  // extern "C"

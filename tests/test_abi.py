@@ -1,0 +1,136 @@
+"""Host-side tests of the C ABI (include/regenvc_attn.h): the library loads,
+exports every declared entry point, and rejects bad arguments synchronously,
+before any HIP call.  The fake device addresses used here are never
+dereferenced: every case fails validation (or is an empty problem) first."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from conftest import REPO, has_gpu_node
+from paper_2607_28144_amd import _lib
+
+HEADER = os.path.join(REPO, "include", "regenvc_attn.h")
+FAKE = 0x10000000  # 16-byte aligned, never dereferenced
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:regenvc_status|const char \*)\s*(regenvc_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ["regenvc_attn_fwd", "regenvc_attn_partial_fwd", "regenvc_lse_merge", "regenvc_cross_attn_fwd",
+              "regenvc_status_str", "regenvc_last_error"]:
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), f"{name} declared in the header but not exported"
+
+
+def test_status_strings(lib):
+    assert lib.regenvc_status_str(0) == b"ok"
+    assert b"invalid" in lib.regenvc_status_str(1)
+    assert lib.regenvc_status_str(2) == b"unsupported"
+    assert b"HIP" in lib.regenvc_status_str(3)
+
+
+def T(ptr=FAKE, sb=None, ss=None, sh=None, S=64, H=2, D=128):
+    """Token-major [B,S,H,D] descriptor at a fake address."""
+    return _lib.Tensor(ptr, S * H * D if sb is None else sb, H * D if ss is None else ss, D if sh is None else sh)
+
+
+def attn(lib, q=None, k=None, v=None, o=None, dtype=_lib.BF16, lse=None, B=1, H=2, Sq=64, Skv=64, D=128,
+         scale=0.088, fn="regenvc_attn_fwd"):
+    q = q if q is not None else T(FAKE, S=Sq, H=H, D=D)
+    k = k if k is not None else T(FAKE + 0x1000000, S=Skv, H=H, D=D)
+    v = v if v is not None else T(FAKE + 0x2000000, S=Skv, H=H, D=D)
+    o = o if o is not None else T(FAKE + 0x3000000, S=Sq, H=H, D=D)
+    byref = lambda t: ctypes.byref(t) if t is not False else None  # noqa: E731
+    if fn == "regenvc_attn_partial_fwd":
+        return lib.regenvc_attn_partial_fwd(byref(q), byref(k), byref(v), byref(o), lse, B, H, Sq, Skv, D,
+                                            scale, None)
+    return getattr(lib, fn)(byref(q), byref(k), byref(v), byref(o), dtype, lse, B, H, Sq, Skv, D, scale, None)
+
+
+def expect(lib, status, want, fragment=None):
+    assert status == want, (status, lib.regenvc_last_error())
+    if want != _lib.OK and fragment is not None:
+        assert fragment in lib.regenvc_last_error().decode(), lib.regenvc_last_error()
+
+
+@pytest.mark.parametrize("fn", ["regenvc_attn_fwd", "regenvc_cross_attn_fwd", "regenvc_attn_partial_fwd"])
+def test_invalid_arguments_are_rejected_before_any_launch(lib, fn):
+    LSE = FAKE + 0x4000000
+    kw = dict(fn=fn, lse=LSE if fn == "regenvc_attn_partial_fwd" else None)
+    expect(lib, attn(lib, q=False, **kw), _lib.ERR_INVALID_ARG, "NULL")
+    expect(lib, attn(lib, q=T(0), **kw), _lib.ERR_INVALID_ARG, "NULL")
+    expect(lib, attn(lib, B=-1, **kw), _lib.ERR_INVALID_ARG, "negative")
+    expect(lib, attn(lib, Sq=-5, **kw), _lib.ERR_INVALID_ARG, "negative")
+    expect(lib, attn(lib, Skv=-1, **kw), _lib.ERR_INVALID_ARG, "key count")
+    expect(lib, attn(lib, D=96, **kw), _lib.ERR_UNSUPPORTED, "head dim")
+    expect(lib, attn(lib, D=256, **kw), _lib.ERR_UNSUPPORTED, "head dim")
+    expect(lib, attn(lib, scale=float("nan"), **kw), _lib.ERR_INVALID_ARG, "finite")
+    expect(lib, attn(lib, scale=float("inf"), **kw), _lib.ERR_INVALID_ARG, "finite")
+    expect(lib, attn(lib, scale=-0.5, **kw), _lib.ERR_INVALID_ARG, "negative")
+    expect(lib, attn(lib, q=T(FAKE + 8), **kw), _lib.ERR_UNSUPPORTED, "aligned")
+    expect(lib, attn(lib, k=T(FAKE + 0x1000000, ss=260), **kw), _lib.ERR_UNSUPPORTED, "multiple of 8")
+    expect(lib, attn(lib, o=T(FAKE), **kw), _lib.ERR_INVALID_ARG, "overlaps")  # o on top of q
+    expect(lib, attn(lib, o=T(FAKE + 0x3000000, ss=0), **kw), _lib.ERR_INVALID_ARG, "overlapping rows")
+    expect(lib, attn(lib, o=T(FAKE + 0x3000000, sb=0, ss=128, sh=64), B=1, **kw), _lib.ERR_INVALID_ARG,
+           "overlapping rows")  # heads interleaved into one another
+    expect(lib, attn(lib, k=T(FAKE + 0x1000000, ss=-(2 ** 62)), Skv=64, **kw), _lib.ERR_UNSUPPORTED, "overflow")
+    if fn != "regenvc_attn_partial_fwd":
+        expect(lib, attn(lib, Skv=0, **kw), _lib.ERR_INVALID_ARG, "key count")
+        expect(lib, attn(lib, dtype=7, **kw), _lib.ERR_INVALID_ARG, "dtype")
+        expect(lib, attn(lib, lse=FAKE + 0x3000000 + 4, fn=fn), _lib.ERR_INVALID_ARG, "lse overlaps")
+        expect(lib, attn(lib, lse=FAKE + 0x4000002, fn=fn), _lib.ERR_UNSUPPORTED, "aligned")
+    else:
+        expect(lib, attn(lib, fn=fn, lse=None), _lib.ERR_INVALID_ARG, "required")
+
+
+@pytest.mark.parametrize("fn", ["regenvc_attn_fwd", "regenvc_cross_attn_fwd", "regenvc_attn_partial_fwd"])
+def test_empty_problems_succeed_without_touching_memory(lib, fn):
+    LSE = FAKE + 0x4000000
+    for B, H, Sq in [(0, 2, 64), (1, 0, 64), (1, 2, 0)]:
+        expect(lib, attn(lib, B=B, H=H, Sq=Sq, fn=fn, lse=LSE), _lib.OK)
+    assert lib.regenvc_last_error() == b""
+
+
+def merge(lib, n=2, o=None, lse=None, parts=None, lparts=None, dtype=_lib.BF16, B=1, H=2, Sq=64, D=128):
+    o = o if o is not None else T(FAKE + 0x3000000, S=Sq, H=H, D=D)
+    size = B * Sq * H * D * 4
+    parts = parts if parts is not None else [FAKE + 0x5000000 + i * 0x1000000 for i in range(max(n, 0))]
+    lparts = lparts if lparts is not None else [FAKE + 0x20000000 + i * 0x100000 for i in range(max(n, 0))]
+    assert size < 0x1000000
+    pa = (ctypes.c_void_p * max(len(parts), 1))(*parts)
+    la = (ctypes.c_void_p * max(len(lparts), 1))(*lparts)
+    return lib.regenvc_lse_merge(pa, la, n, ctypes.byref(o), dtype, lse, B, H, Sq, D, None)
+
+
+def test_merge_validation(lib):
+    expect(lib, merge(lib, n=0), _lib.ERR_INVALID_ARG, "num_parts")
+    expect(lib, merge(lib, n=17, parts=[FAKE] * 17, lparts=[FAKE] * 17), _lib.ERR_INVALID_ARG, "num_parts")
+    expect(lib, merge(lib, parts=[FAKE + 0x5000000, 0]), _lib.ERR_INVALID_ARG, "NULL")
+    expect(lib, merge(lib, parts=[FAKE + 0x5000008, FAKE + 0x6000000]), _lib.ERR_UNSUPPORTED, "aligned")
+    expect(lib, merge(lib, D=32), _lib.ERR_UNSUPPORTED, "head dim")
+    expect(lib, merge(lib, dtype=3), _lib.ERR_INVALID_ARG, "dtype")
+    expect(lib, merge(lib, o=T(FAKE + 0x5000000)), _lib.ERR_INVALID_ARG, "overlaps part")
+    expect(lib, merge(lib, lse=FAKE + 0x20000000), _lib.ERR_INVALID_ARG, "overlaps part")
+    expect(lib, merge(lib, o=T(FAKE + 0x3000000, ss=0)), _lib.ERR_INVALID_ARG, "overlapping rows")
+    expect(lib, merge(lib, B=0), _lib.OK)
+
+
+@pytest.mark.skipif(has_gpu_node(), reason="would reach a launch on fake addresses on a GPU machine")
+def test_valid_arguments_without_a_gpu_report_a_hip_error(lib):
+    # Validation passes, then the device query fails: nothing can be launched.
+    expect(lib, attn(lib), _lib.ERR_HIP, "hip")
