@@ -76,13 +76,35 @@ def cpu_baseline(target_s: float):
     }
 
 
+def copy_reference(torch, dev, args):
+    """Plain elementwise copy (out = -in) of 1 GiB float32: reads 1 GiB and
+    writes 1 GiB per launch.  Its FETCH_SIZE / WRITE_SIZE readings calibrate
+    the counters of the attention kernels."""
+    n = 1 << 28
+    a = torch.randn(n, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(args.warmup):
+        torch.neg(a, out=b)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        torch.neg(a, out=b)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "ms": ms,
+                      "GB/s": 8 * n / (ms * 1e-3) / 1e9}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--only", choices=["self", "cross", "share"], default=None,
-                    help="time one component alone (for profiling)")
+    ap.add_argument("--only", choices=["self", "cross", "share", "copy"], default=None,
+                    help="time one component alone (for profiling); 'copy' runs a plain 1 GiB elementwise "
+                         "copy kernel, the reference for scaling HBM byte counters")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle sample")
     args = ap.parse_args()
@@ -100,6 +122,9 @@ def main():
         sys.exit(2)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.only == "copy":
+        copy_reference(torch, dev, args)
+        return
 
     def to_dev(bits):
         return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
