@@ -12,7 +12,7 @@ REPO_DIR = os.path.dirname(PKG_DIR)
 CSRC = os.path.join(PKG_DIR, "csrc")
 LIB_NAME = "libregenvc_attn.so"
 LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
-SOURCES = ["api.cpp", "attn_fwd.hip"]
+SOURCES = ["api.cpp", "attn_fwd.hip", "lse_merge.hip"]
 ARCH = "gfx950"
 
 
@@ -33,6 +33,9 @@ def build(verbose: bool = False) -> str:
         "-shared",
         "-Wall",
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+        # MFMA results in VGPRs: the score tiles feed VALU softmax code directly,
+        # and read-only operands may then live in AGPRs
+        "-mllvm", "-amdgpu-mfma-vgpr-form",
         "-I", os.path.join(REPO_DIR, "include"),
         "-I", CSRC,
         "-o", out_tmp,

@@ -1,5 +1,5 @@
 // gfx950 blockwise exact attention: bf16 MFMA for Q K^T and P V with fp32
-// accumulation, online softmax in registers, K/V tiles double-buffered in LDS.
+// accumulation, online softmax in registers, K/V tiles streamed through LDS.
 //
 // Method: exact softmax attention computed blockwise over key/value tiles with
 // a running (max, sum) per query row -- the "online-softmax" combination the
@@ -7,11 +7,15 @@
 // GPU's share (a subset of heads, all or a chunk of the keys).
 //
 // Work decomposition
-//   workgroup = 4 waves = one (batch, head, BM-query tile); BM = 4 * 32 * QB.
-//   wave      = QB blocks of 32 queries, all head dims, every key tile.
-//   key tile  = 64 keys; K and V tiles live in LDS, two buffers.
+//   workgroup = 4 waves = one (batch, head, 256-query tile); one per CU.
+//   wave      = 64 queries (two 32-query blocks), all head dims, every key tile.
+//   key tile  = 32 keys.  K and V tiles are copied HBM -> LDS with
+//               global_load_lds_dwordx4 (no register staging) into a 4-stage
+//               ring: three tiles in flight, one barrier per tile.
+//   Workgroups are renumbered so that the tiles of one head run on the same
+//   XCD (each XCD has its own L2; the hardware deals workgroups round-robin).
 //
-// Layout trick: scores are computed transposed, S^T = K Q^T, with the MFMA
+// Layout trick: scores are computed transposed, S^T = K Q^T, with
 //   v_mfma_f32_32x32x16_bf16 (A = 32 keys x 16 dims from LDS, B = 16 dims x
 //   32 queries held in registers).  In the 32x32 accumulator a lane owns ONE
 //   query column and 16 of the 32 keys, so row max / row sum are in-register
@@ -21,89 +25,215 @@
 //   with ds_read_b64_tr_b16 in that key order.  Attention is invariant under
 //   a joint permutation of keys and values, so no shuffle is needed.
 //
+// Software pipeline (per wave, tile t):
+//   phase X:  MFMA  S_{t+1} = K_{t+1} Q^T (both query blocks)
+//             VALU  softmax of S_t, query block 1
+//   phase Y:  MFMA  O^T += V_t^T P_t^T (both query blocks)
+//             VALU  softmax of S_{t+1}, query block 0
+//   so the exponentials of one half always run beside the other half's MFMAs.
+//
 // Lazy rescaling: the running max used as the exponent reference is only
 //   raised when a tile's max exceeds it by more than 8 (log2 units); the
 //   exponentials are then bounded by 2^8, which fp32 sums and bf16 operands
-//   hold exactly as well as values <= 1.  The final O / l and
+//   hold as well as values <= 1.  The final O / l and
 //   LSE = ln2 * (m_ref + log2 l) are the same quantities for any reference,
-//   so this only removes the O-rescale work from the common path.
+//   so this only removes the O-rescale work from the common path; when it is
+//   needed it is applied between the phases, outside the MFMA streams.
 #include "attn_kernels.hpp"
 
 #include <math.h>
+
+#include <type_traits>
 
 namespace regenvc {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-typedef __attribute__((address_space(3))) uint16_t lds_u16;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+typedef __attribute__((address_space(3))) char lds_char;
 
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kBlockN = 64;                 // keys per tile
-constexpr float kRescaleThreshold = 8.0f;  // log2 units
+constexpr int kBlockN = 32;                 // keys per tile
+constexpr int kStages = 4;                  // LDS ring depth
+constexpr int kAhead = kStages - 1;         // tiles in flight
+constexpr float kRescaleThreshold = 8.0f;   // log2 units
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-// LDS placement of 16-byte chunk `ch` of tile row `row`.  K rows are read
-// 16 B per lane, 32 consecutive rows at one chunk: XOR with the row spreads
-// them over distinct banks.  V rows are read with the 8-byte transposing
-// load, 4 consecutive rows x 2 adjacent chunks per 16 lanes: XOR with 4*(row%4)
-// keeps those 8 (and, with the neighbouring 16 lanes, 16) chunks distinct.
+template <int D>
+struct Geo {
+    static constexpr int NCH = D / 8;                      // 16-byte chunks per row
+    static constexpr int DS = D / 16;                      // k-steps of Q K^T
+    static constexpr int DB = D / 32;                      // 32-row blocks of O^T
+    static constexpr int TILE = kBlockN * D * 2;           // bytes of one K or V tile
+    static constexpr int STAGE = 2 * TILE;                 // K tile then V tile
+    static constexpr int LDS = kStages * STAGE;
+    static constexpr int LOADS = kBlockN * NCH / kThreads; // 16-byte loads per thread per tensor per tile
+    static_assert(LOADS >= 1 && (kBlockN * NCH) % kThreads == 0, "tile load split");
+};
+
+// LDS placement of 16-byte chunk `ch` of tile row `row` (an involution in ch).
+// K rows are read 16 B per lane, 32 consecutive rows at one chunk: XOR with the
+// row spreads them over distinct banks.  V rows are read with the 8-byte
+// transposing load, 4 consecutive rows x 2 adjacent chunks per 16 lanes: XOR
+// with 4*(row%4) keeps those 8 (and, with the neighbouring 16 lanes, 16)
+// chunks distinct.
 template <int NCH>
 __device__ __forceinline__ int k_slot(int row, int ch) { return ch ^ (row & (NCH - 1)); }
 template <int NCH>
 __device__ __forceinline__ int v_slot(int row, int ch) { return ch ^ ((4 * (row & 3)) & (NCH - 1)); }
 
+// 16-byte HBM -> LDS copy (global_load_lds_dwordx4): lane i's 16 bytes land at
+// lds_base + 16 * i.  Written as inline asm so the compiler does not treat it
+// as an LDS store it must wait for before every later LDS read (it cannot
+// tell the ring stages apart); completion is awaited explicitly with
+// s_waitcnt vmcnt before the barrier that publishes a stage.
+__device__ __forceinline__ void lds_dma16(const void *gptr, uint32_t lds_base)
+{
+    const uint32_t base = __builtin_amdgcn_readfirstlane(lds_base);  // wave-uniform by construction
+    __asm__ volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" : : "s"(base), "v"(gptr) : "m0");
+}
+
 // (x of this lane, x of lane^32) combined so both halves hold the same value.
-__device__ __forceinline__ float pair_max(float x) {
+__device__ __forceinline__ float pair_max(float x)
+{
     auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
-__device__ __forceinline__ float pair_sum(float x) {
+__device__ __forceinline__ float pair_sum(float x)
+{
     auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-template <int D, int QB, bool OUT_F32>
+// Instruction interleaving for the two pipeline phases (scheduler groups:
+// 0x008 MFMA, 0x002 VALU, 0x100 LDS read).  Each 32-cycle MFMA is followed
+// by a few independent VALU softmax instructions, and the LDS fragment reads
+// run a few MFMAs ahead of their use.
+template <int NFRAG>
+__device__ __forceinline__ void sched_phase_x()
+{
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+    for (int i = 0; i < NFRAG; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+    }
+}
+template <int NFRAG>
+__device__ __forceinline__ void sched_phase_y()
+{
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int i = 0; i < NFRAG; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+    }
+}
+
+// Online-softmax step for one 32-query block over one 32-key tile.
+//   s      : S^T accumulator of the tile (raw q.k dot products); register i
+//            holds key (i/4)*8 + hi*4 + i%4 of the tile for this lane's query
+//   c      : scale * log2(e)
+//   mref   : exponent reference (log2 units), raised lazily
+//   lsum   : running fp32 sum of exp2(s*c - mref) over this lane's keys (the
+//            unrounded weights: summing the bf16-rounded ones would move LSE
+//            by up to 2^-9 when few keys dominate)
+//   p      : bf16 P^T operands of the two 16-key MFMA steps of the tile
+//   alpha  : factor the O accumulator must be multiplied by (1 if unchanged)
+//   upd    : wave-uniform flag: some lane raised its reference
+// MASK: keys at or past Skv (only in the last tile) get weight exactly 0.
+template <bool MASK>
+__device__ __forceinline__ void softmax_block(const f32x16 &s, float c, float &mref, float &lsum,
+                                              bf16x8 (&p)[2], float &alpha, bool &upd, int key0, int Skv)
+{
+    const int hi = (threadIdx.x >> 5) & 1;
+    auto valid = [&](int i) { return key0 + (i >> 2) * 8 + hi * 4 + (i & 3) < Skv; };
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, (!MASK || valid(i)) ? s[i] : -INFINITY);
+    const float mt = pair_max(mx) * c;
+    upd = __builtin_amdgcn_ballot_w64(mt > mref + kRescaleThreshold) != 0;
+    const float mnew = upd ? fmaxf(mref, mt) : mref;
+    alpha = __builtin_amdgcn_exp2f(mref - mnew);
+    mref = mnew;
+    const float nm = -mnew;
+    float acc0 = 0.f, acc1 = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; i += 2) {
+        float e0 = __builtin_amdgcn_exp2f(fmaf(s[i], c, nm));
+        float e1 = __builtin_amdgcn_exp2f(fmaf(s[i + 1], c, nm));
+        if (MASK) {
+            e0 = valid(i) ? e0 : 0.f;
+            e1 = valid(i + 1) ? e1 : 0.f;
+        }
+        bf16x2 pk;
+        pk[0] = (__bf16)e0;
+        pk[1] = (__bf16)e1;
+        p[i >> 3][i & 7] = pk[0];
+        p[i >> 3][(i & 7) + 1] = pk[1];
+        acc0 += e0;
+        acc1 += e1;
+    }
+    lsum = fmaf(lsum, alpha, acc0 + acc1);
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt()
+{
+    __asm__ volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+template <int D, bool OUT_F32>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attn_fwd_kernel(AttnArgs a, int n_qtiles)
 {
-    constexpr int NCH = D / 8;    // 16-byte chunks per row
-    constexpr int DS = D / 16;    // k-steps of the Q K^T MFMA
-    constexpr int DB = D / 32;    // 32-row blocks of O^T
-    constexpr int BM = kWaves * 32 * QB;
-    constexpr int LOADS = kBlockN * NCH / kThreads;  // 16-byte chunks per thread per tile
-    static_assert(LOADS >= 1 && (kBlockN * NCH) % kThreads == 0, "tile load split");
+    using G = Geo<D>;
+    constexpr int NCH = G::NCH, DS = G::DS, DB = G::DB, LOADS = G::LOADS;
+    constexpr int BM = kWaves * 64;
+    constexpr int PER_TILE = 2 * LOADS;  // copies in flight per thread per tile (K and V)
 
-    __shared__ __attribute__((aligned(16))) uint16_t smem[2][2][kBlockN * D];  // [buf][K|V]
+    __shared__ __attribute__((aligned(1024))) char smem[G::LDS];
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int hi = lane >> 5;   // which half of the wave
     const int col = lane & 31;  // query column owned in the 32x32 accumulators
 
-    int bid = blockIdx.x;
+    // XCD-aware renumbering: workgroup i runs on XCD i % 8; give each XCD a
+    // contiguous range of (b, h, q-tile) so one head's tiles share an L2.
+    const int nwg = gridDim.x;
+    const int xcd = blockIdx.x & 7;
+    int bid = xcd * (nwg >> 3) + min(xcd, nwg & 7) + (blockIdx.x >> 3);
     const int qt = bid % n_qtiles;
     bid /= n_qtiles;
     const int h = bid % a.H;
     const int b = bid / a.H;
-    const int q0 = qt * BM + wave * 32 * QB;
+    const int q0 = qt * BM + wave * 64;
 
     const uint16_t *qp = static_cast<const uint16_t *>(a.q) + b * a.q_sb + h * a.q_sh;
     const uint16_t *kp = static_cast<const uint16_t *>(a.k) + b * a.k_sb + h * a.k_sh;
     const uint16_t *vp = static_cast<const uint16_t *>(a.v) + b * a.v_sb + h * a.v_sh;
     const int Sq = a.Sq, Skv = a.Skv;
+    const int nt = (Skv + kBlockN - 1) / kBlockN;
+    const bool ragged = (Skv % kBlockN) != 0;
 
     // Q^T operand fragments stay in registers for the whole key loop.
-    bf16x8 qf[QB][DS];
+    bf16x8 qf[2][DS];
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
+    for (int qb = 0; qb < 2; ++qb) {
         const int qi = q0 + qb * 32 + col;
 #pragma unroll
         for (int ds = 0; ds < DS; ++ds) {
@@ -114,154 +244,159 @@ void attn_fwd_kernel(AttnArgs a, int n_qtiles)
         }
     }
 
-    f32x16 oacc[QB][DB];
-    float mref[QB], lsum[QB];
+    // HBM -> LDS copy of key tile `tile` (clamped to the last tile) into its
+    // ring stage.  Each wave instruction fills 1 KB of LDS (64 lanes x 16 B,
+    // in lane order); the lane fetches the chunk the swizzle places there.
+    // Rows past the last key re-read the last key (finite data; their softmax
+    // weight is 0).  Every call issues exactly PER_TILE copies per thread, so
+    // the vmcnt waits below count whole tiles.
+    auto issue_loads = [&](int tile) {
+        tile = min(tile, nt - 1);
+        const uint32_t kdst = (uint32_t)(uintptr_t)(lds_char *)(smem + (tile % kStages) * G::STAGE);
+        const uint32_t vdst = kdst + G::TILE;
+        const int key0 = tile * kBlockN;
+        const int last = Skv - 1 - key0;
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-        mref[qb] = -INFINITY;
-        lsum[qb] = 0.f;
+        for (int j = 0; j < LOADS; ++j) {
+            const int blk = wave * LOADS + j;
+            const int slot = blk * 64 + lane;
+            const int row = slot / NCH, phys = slot % NCH;
+            const int64_t key = key0 + min(row, last);
+            const uint16_t *gk = kp + key * a.k_ss + k_slot<NCH>(row, phys) * 8;
+            const uint16_t *gv = vp + key * a.v_ss + v_slot<NCH>(row, phys) * 8;
+            lds_dma16(gk, kdst + blk * 1024);
+            lds_dma16(gv, vdst + blk * 1024);
+        }
+    };
+
+    // Per-lane LDS byte offsets of the MFMA operand fragments (stage 0).
+    int koff[DS];
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) koff[ds] = (col * D + k_slot<NCH>(col, ds * 2 + hi) * 8) * 2;
+    const int g = lane >> 4, x = lane & 15;
+    int voff[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+        const int row = 4 * (g >> 1) + (x >> 2);
+        const int dcol = db * 32 + 16 * (g & 1) + 4 * (x & 3);
+        voff[db] = G::TILE + (row * D + v_slot<NCH>(row, dcol >> 3) * 8 + (dcol & 7)) * 2;
+    }
+
+    // S^T of both query blocks from the K tile of `tile`.
+    auto qk = [&](int tile, f32x16 (&s)[2]) {
+        const lds_char *kt = (const lds_char *)(smem + (tile % kStages) * G::STAGE);
+        s[0] = s[1] = f32x16{};
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds) {
+            const bf16x8 kf = *(const lds_bf16x8 *)(kt + koff[ds]);
+            s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[0][ds], s[0], 0, 0, 0);
+            s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[1][ds], s[1], 0, 0, 0);
+        }
+    };
+
+    f32x16 oacc[2][DB];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
         for (int db = 0; db < DB; ++db) oacc[qb][db] = f32x16{};
-    }
-    const float c = a.scale * kLog2e;
-    const int ntiles = (Skv + kBlockN - 1) / kBlockN;
 
-    u32x4 kreg[LOADS], vreg[LOADS];
-    auto gload = [&](int tile) {
+    // O^T += V^T P^T for both query blocks from the V tile of `tile`.  MFMA
+    // k-step kk covers tile keys 16kk..16kk+15; the lower half-wave supplies
+    // keys {0-3, 8-11}, the upper {4-7, 12-15} (the S^T accumulator order).
+    auto pv = [&](int tile, const bf16x8 (&p0)[2], const bf16x8 (&p1)[2]) {
+        const lds_char *vt = (const lds_char *)(smem + (tile % kStages) * G::STAGE);
 #pragma unroll
-        for (int j = 0; j < LOADS; ++j) {
-            const int id = threadIdx.x + j * kThreads;
-            const int row = id / NCH, ch = id % NCH;
-            const int key = tile * kBlockN + row;
-            if (key < Skv) {
-                kreg[j] = *reinterpret_cast<const u32x4 *>(kp + (int64_t)key * a.k_ss + ch * 8);
-                vreg[j] = *reinterpret_cast<const u32x4 *>(vp + (int64_t)key * a.v_ss + ch * 8);
-            } else {  // keys past the end: finite zeros, masked out of the softmax below
-                kreg[j] = u32x4{};
-                vreg[j] = u32x4{};
-            }
-        }
-    };
-    auto lstore = [&](int buf) {
-#pragma unroll
-        for (int j = 0; j < LOADS; ++j) {
-            const int id = threadIdx.x + j * kThreads;
-            const int row = id / NCH, ch = id % NCH;
-            *reinterpret_cast<u32x4 *>(&smem[buf][0][row * D + k_slot<NCH>(row, ch) * 8]) = kreg[j];
-            *reinterpret_cast<u32x4 *>(&smem[buf][1][row * D + v_slot<NCH>(row, ch) * 8]) = vreg[j];
-        }
-    };
-
-    gload(0);
-    lstore(0);
-    for (int t = 0; t < ntiles; ++t) {
-        __syncthreads();  // tile t visible in buffer t&1; buffer (t+1)&1 free
-        const int buf = t & 1;
-        if (t + 1 < ntiles) gload(t + 1);
-
-        // S^T = K Q^T for two 32-key blocks
-        f32x16 sacc[QB][2];
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) sacc[qb][0] = sacc[qb][1] = f32x16{};
-        const uint16_t *kt = smem[buf][0];
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            const int row = kb * 32 + col;
-#pragma unroll
-            for (int ds = 0; ds < DS; ++ds) {
-                const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(kt + row * D + k_slot<NCH>(row, ds * 2 + hi) * 8);
-#pragma unroll
-                for (int qb = 0; qb < QB; ++qb)
-                    sacc[qb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][ds], sacc[qb][kb], 0, 0, 0);
-            }
-        }
-
-        // Keys of this lane: accumulator register i of block kb holds key
-        // kb*32 + (i/4)*8 + hi*4 + i%4 of the tile.
-        const bool ragged = (t + 1) * kBlockN > Skv;
-        const int kbase = t * kBlockN + hi * 4;
-
-        float mt[QB];
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-            float mx = -INFINITY;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int key = kbase + kb * 32 + (i >> 2) * 8 + (i & 3);
-                    const float x = (ragged && key >= Skv) ? -INFINITY : sacc[qb][kb][i];
-                    mx = fmaxf(mx, x);
-                }
-            mt[qb] = pair_max(mx) * c;
-        }
-        bool need = false;
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) need |= mt[qb] > mref[qb] + kRescaleThreshold;
-        if (__builtin_amdgcn_ballot_w64(need) != 0) {
-#pragma unroll
-            for (int qb = 0; qb < QB; ++qb) {
-                const float mnew = fmaxf(mref[qb], mt[qb]);
-                const float alpha = __builtin_amdgcn_exp2f(mref[qb] - mnew);
-                lsum[qb] *= alpha;
-#pragma unroll
-                for (int db = 0; db < DB; ++db) oacc[qb][db] *= alpha;
-                mref[qb] = mnew;
-            }
-        }
-
-        // P^T fragments (bf16) and row sums.
-        bf16x8 pf[QB][4];
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-            const float nm = -mref[qb];
-            float ls = 0.f;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int key = kbase + kb * 32 + (i >> 2) * 8 + (i & 3);
-                    float p = __builtin_amdgcn_exp2f(fmaf(sacc[qb][kb][i], c, nm));
-                    if (ragged && key >= Skv) p = 0.f;
-                    ls += p;
-                    pf[qb][kb * 2 + (i >> 3)][i & 7] = (__bf16)p;
-                }
-            lsum[qb] += ls;
-        }
-
-        // O^T += V^T P^T.  MFMA k-step kk covers tile keys 16kk..16kk+15; the
-        // lower half-wave supplies keys {0-3, 8-11}, the upper {4-7, 12-15}.
-        const uint16_t *vt = smem[buf][1];
-        const int g = lane >> 4, x = lane & 15;
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
+        for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
-                const int dcol = db * 32 + 16 * (g & 1) + 4 * (x & 3);  // first of 4 dims this lane fetches
-                bf16x8 vf;
+                const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                    (lds_bf16x4 *)(vt + voff[db] + kk * 16 * D * 2));
+                const bf16x4 up = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                    (lds_bf16x4 *)(vt + voff[db] + (kk * 16 + 8) * D * 2));
+                const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
+                oacc[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, p0[kk], oacc[0][db], 0, 0, 0);
+                oacc[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, p1[kk], oacc[1][db], 0, 0, 0);
+            }
+    };
+
+    const float c = a.scale * kLog2e;
+    float mref[2] = {-INFINITY, -INFINITY};
+    float lsum[2] = {0.f, 0.f};
+    f32x16 scur1, snext[2];
+    bf16x8 p0cur[2], p0next[2], p1[2];
+    float alpha0 = 1.f, alpha1 = 1.f;
+    bool upd0 = false, upd1 = false;
+
+    // Prologue: kAhead tiles in flight; S_0 and the softmax of its block 0.
 #pragma unroll
-                for (int half = 0; half < 2; ++half) {
-                    const int row = kk * 16 + 4 * (g >> 1) + 8 * half + (x >> 2);
-                    const int off = row * D + v_slot<NCH>(row, dcol >> 3) * 8 + (dcol & 7);
-                    const bf16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-                        (lds_bf16x4 *)((lds_u16 *)vt + off));
-                    vf[half * 4 + 0] = r[0];
-                    vf[half * 4 + 1] = r[1];
-                    vf[half * 4 + 2] = r[2];
-                    vf[half * 4 + 3] = r[3];
-                }
+    for (int i = 0; i < kAhead; ++i) issue_loads(i);
+    wait_vmcnt<(kAhead - 1) * PER_TILE>();
+    __syncthreads();
+    {
+        f32x16 s0[2];
+        qk(0, s0);
+        if (nt == 1 && ragged)
+            softmax_block<true>(s0[0], c, mref[0], lsum[0], p0cur, alpha0, upd0, 0, Skv);
+        else
+            softmax_block<false>(s0[0], c, mref[0], lsum[0], p0cur, alpha0, upd0, 0, Skv);
+        scur1 = s0[1];
+    }
+    upd0 = false;  // O is still zero: nothing to rescale
+
+    // One tile of the pipeline.  HAS_NEXT: tile t+1 exists (S_{t+1} is
+    // computed here); MASK_NEXT / MASK_CUR: tile t+1 / t is the ragged last one.
+    auto step = [&](int t, auto has_next, auto mask_next, auto mask_cur) {
+        constexpr bool HAS_NEXT = decltype(has_next)::value;
+        constexpr bool MASK_NEXT = decltype(mask_next)::value;
+        constexpr bool MASK_CUR = decltype(mask_cur)::value;
+        // ---- phase X
+        if constexpr (HAS_NEXT) {
+            wait_vmcnt<(kAhead - 2) * PER_TILE>();  // this wave's copies of tile t+1 landed
+            __syncthreads();                         // ... and every other wave's
+            issue_loads(t + kAhead);                 // into the stage tile t-1 used
+            qk(t + 1, snext);
+        }
+        softmax_block<MASK_CUR>(scur1, c, mref[1], lsum[1], p1, alpha1, upd1, t * kBlockN, Skv);
+        if constexpr (HAS_NEXT) {
+            sched_phase_x<DS / 2>();
+            // keep the block-1 softmax in this phase (not sunk next to its use)
+            __asm__ volatile("" : : "v"(p1[0]), "v"(p1[1]), "v"(lsum[1]));
+        }
+        // ---- deferred O rescale (rare): between the two MFMA streams
+        if (upd0 || upd1) {
 #pragma unroll
-                for (int qb = 0; qb < QB; ++qb)
-                    oacc[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qb][kk], oacc[qb][db], 0, 0, 0);
+            for (int db = 0; db < DB; ++db) {
+                oacc[0][db] *= (upd0 ? alpha0 : 1.f);
+                oacc[1][db] *= (upd1 ? alpha1 : 1.f);
             }
         }
+        upd0 = false;
+        // ---- phase Y
+        pv(t, p0cur, p1);
+        if constexpr (HAS_NEXT) {
+            softmax_block<MASK_NEXT>(snext[0], c, mref[0], lsum[0], p0next, alpha0, upd0, (t + 1) * kBlockN, Skv);
+            scur1 = snext[1];
+            p0cur[0] = p0next[0];
+            p0cur[1] = p0next[1];
+            sched_phase_y<DB>();
+        }
+    };
 
-        if (t + 1 < ntiles) lstore((t + 1) & 1);
+    using T_ = std::true_type;
+    using F_ = std::false_type;
+    const int n_plain = ragged ? nt - 2 : nt - 1;  // tiles with a successor and no masking anywhere
+    for (int t = 0; t < n_plain; ++t) step(t, T_{}, F_{}, F_{});
+    if (ragged) {
+        if (nt >= 2) step(nt - 2, T_{}, T_{}, F_{});
+        step(nt - 1, F_{}, F_{}, T_{});
+    } else {
+        step(nt - 1, F_{}, F_{}, F_{});
     }
+    wait_vmcnt<0>();  // the clamped trailing copies must land before the workgroup exits
 
     // Epilogue: O = O^T / l, LSE = ln2 * (m_ref + log2 l).
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
+    for (int qb = 0; qb < 2; ++qb) {
         const float lt = pair_sum(lsum[qb]);
         const float inv = 1.0f / lt;
         const int qi = q0 + qb * 32 + col;
@@ -291,111 +426,25 @@ void attn_fwd_kernel(AttnArgs a, int n_qtiles)
     }
 }
 
-template <int D, int QB, bool OUT_F32>
+template <int D, bool OUT_F32>
 hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream)
 {
-    constexpr int BM = kWaves * 32 * QB;
+    constexpr int BM = kWaves * 64;
     const int n_qtiles = (a.Sq + BM - 1) / BM;
     const int64_t nblocks = (int64_t)n_qtiles * a.H * a.B;
     if (nblocks > 0x7fffffff) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((attn_fwd_kernel<D, QB, OUT_F32>), dim3((unsigned)nblocks), dim3(kThreads), 0, stream, a,
+    hipLaunchKernelGGL((attn_fwd_kernel<D, OUT_F32>), dim3((unsigned)nblocks), dim3(kThreads), 0, stream, a,
                        n_qtiles);
     return hipGetLastError();
-}
-
-// ---------------------------------------------------------------------------
-// Log-sum-exp merge of chunk partials: one thread per 4 dims of one row.
-template <bool OUT_F32>
-__global__ __launch_bounds__(256) void lse_merge_kernel(MergeArgs a)
-{
-    const int per_row = a.D / 4;
-    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t rows = (int64_t)a.B * a.Sq * a.H;
-    const int64_t row = gid / per_row;  // row index in [B, Sq, H] order
-    if (row >= rows) return;
-    const int d = (int)(gid % per_row) * 4;
-    const int h = (int)(row % a.H);
-    const int64_t bi = row / a.H;
-    const int i = (int)(bi % a.Sq);
-    const int b = (int)(bi / a.Sq);
-    const int64_t li = ((int64_t)b * a.H + h) * a.Sq + i;
-
-    float m = -INFINITY;
-    for (int c = 0; c < a.num_parts; ++c) m = fmaxf(m, a.lse_parts[c][li]);
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    float L = -INFINITY;
-    if (m != -INFINITY) {
-        float s = 0.f;
-        for (int c = 0; c < a.num_parts; ++c) s += expf(a.lse_parts[c][li] - m);
-        L = m + logf(s);
-        for (int c = 0; c < a.num_parts; ++c) {
-            const float w = expf(a.lse_parts[c][li] - L);
-            const f32x4 oc = *reinterpret_cast<const f32x4 *>(a.o_parts[c] + row * a.D + d);
-            acc += w * oc;
-        }
-    }
-    char *orow = static_cast<char *>(a.o) + ((int64_t)b * a.o_sb + (int64_t)i * a.o_ss + (int64_t)h * a.o_sh) *
-                                                (OUT_F32 ? 4 : 2);
-    if constexpr (OUT_F32) {
-        *reinterpret_cast<f32x4 *>(orow + d * 4) = acc;
-    } else {
-        bf16x4 w;
-        for (int e = 0; e < 4; ++e) w[e] = (__bf16)acc[e];
-        *reinterpret_cast<bf16x4 *>(orow + d * 2) = w;
-    }
-    if (a.lse != nullptr && d == 0) a.lse[li] = L;
-}
-
-__global__ __launch_bounds__(256) void empty_partial_kernel(FillArgs a)
-{
-    const int per_row = a.D / 4;
-    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t rows = (int64_t)a.B * a.Sq * a.H;
-    const int64_t row = gid / per_row;
-    if (row >= rows) return;
-    const int d = (int)(gid % per_row) * 4;
-    const int h = (int)(row % a.H);
-    const int64_t bi = row / a.H;
-    const int i = (int)(bi % a.Sq);
-    const int b = (int)(bi / a.Sq);
-    float *orow = a.o + (int64_t)b * a.o_sb + (int64_t)i * a.o_ss + (int64_t)h * a.o_sh;
-    *reinterpret_cast<f32x4 *>(orow + d) = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (d == 0) a.lse[((int64_t)b * a.H + h) * a.Sq + i] = -INFINITY;
 }
 
 }  // namespace
 
 hipError_t launch_attn(const AttnArgs &a, hipStream_t stream)
 {
-    if (a.D == 128)
-        return a.o_f32 ? launch_attn_t<128, 2, true>(a, stream) : launch_attn_t<128, 2, false>(a, stream);
-    if (a.D == 64)
-        return a.o_f32 ? launch_attn_t<64, 2, true>(a, stream) : launch_attn_t<64, 2, false>(a, stream);
+    if (a.D == 128) return a.o_f32 ? launch_attn_t<128, true>(a, stream) : launch_attn_t<128, false>(a, stream);
+    if (a.D == 64) return a.o_f32 ? launch_attn_t<64, true>(a, stream) : launch_attn_t<64, false>(a, stream);
     return hipErrorInvalidValue;
-}
-
-static int64_t elementwise_blocks(int64_t rows, int D)
-{
-    return (rows * (D / 4) + 255) / 256;
-}
-
-hipError_t launch_merge(const MergeArgs &a, hipStream_t stream)
-{
-    const int64_t nb = elementwise_blocks((int64_t)a.B * a.Sq * a.H, a.D);
-    if (nb > 0x7fffffff) return hipErrorInvalidConfiguration;
-    if (a.o_f32)
-        hipLaunchKernelGGL(lse_merge_kernel<true>, dim3((unsigned)nb), dim3(256), 0, stream, a);
-    else
-        hipLaunchKernelGGL(lse_merge_kernel<false>, dim3((unsigned)nb), dim3(256), 0, stream, a);
-    return hipGetLastError();
-}
-
-hipError_t launch_empty_partial(const FillArgs &a, hipStream_t stream)
-{
-    const int64_t nb = elementwise_blocks((int64_t)a.B * a.Sq * a.H, a.D);
-    if (nb > 0x7fffffff) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(empty_partial_kernel, dim3((unsigned)nb), dim3(256), 0, stream, a);
-    return hipGetLastError();
 }
 
 }  // namespace regenvc
