@@ -7,11 +7,13 @@
 // GPU's share (a subset of heads, all or a chunk of the keys).
 //
 // Work decomposition
-//   workgroup = 4 waves = one (batch, head, 256-query tile); one per CU.
-//   wave      = 64 queries (two 32-query blocks), all head dims, every key tile.
-//   key tile  = 32 keys.  K and V tiles are copied HBM -> LDS with
-//               global_load_lds_dwordx4 (no register staging) into a 4-stage
-//               ring: three tiles in flight, one barrier per tile.
+//   workgroup = 8 waves = one (batch, head, 256-query tile); one per CU, so
+//               each SIMD runs two waves and one wave's exponentials overlap
+//               the other's matrix instructions.
+//   wave      = 32 queries, all head dims, every key tile.
+//   key tile  = 64 keys.  K and V tiles are copied HBM -> LDS with
+//               global_load_lds_dwordx4 (no register staging) into a 3-stage
+//               ring: two tiles in flight, one barrier per tile.
 //   Workgroups are renumbered so that the tiles of one head run on the same
 //   XCD (each XCD has its own L2; the hardware deals workgroups round-robin).
 //
@@ -26,11 +28,11 @@
 //   a joint permutation of keys and values, so no shuffle is needed.
 //
 // Software pipeline (per wave, tile t):
-//   phase X:  MFMA  S_{t+1} = K_{t+1} Q^T (both query blocks)
-//             VALU  softmax of S_t, query block 1
-//   phase Y:  MFMA  O^T += V_t^T P_t^T (both query blocks)
-//             VALU  softmax of S_{t+1}, query block 0
-//   so the exponentials of one half always run beside the other half's MFMAs.
+//   phase X:  MFMA  S_{t+1} = K_{t+1} Q^T
+//             VALU  softmax of S_t
+//   phase Y:  MFMA  O^T += V_t^T P_t^T
+//   the exponentials of tile t run beside the Q K^T products of tile t+1 (and
+//   beside the other wave's MFMAs on the same SIMD).
 //
 // Lazy rescaling: the running max used as the exponent reference is only
 //   raised when a tile's max exceeds it by more than 8 (log2 units); the
@@ -57,10 +59,10 @@ typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 typedef __attribute__((address_space(3))) char lds_char;
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kBlockN = 32;                 // keys per tile
-constexpr int kStages = 4;                  // LDS ring depth
+constexpr int kBlockN = 64;                 // keys per tile
+constexpr int kStages = 3;                  // LDS ring depth
 constexpr int kAhead = kStages - 1;         // tiles in flight
 constexpr float kRescaleThreshold = 8.0f;   // log2 units
 constexpr float kLog2e = 1.4426950408889634f;
@@ -112,59 +114,32 @@ __device__ __forceinline__ float pair_sum(float x)
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Instruction interleaving for the two pipeline phases (scheduler groups:
-// 0x008 MFMA, 0x002 VALU, 0x100 LDS read).  Each 32-cycle MFMA is followed
-// by a few independent VALU softmax instructions, and the LDS fragment reads
-// run a few MFMAs ahead of their use.
-template <int NFRAG>
-__device__ __forceinline__ void sched_phase_x()
-{
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-#pragma unroll
-    for (int i = 0; i < NFRAG; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
-    }
-}
-template <int NFRAG>
-__device__ __forceinline__ void sched_phase_y()
-{
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-#pragma unroll
-    for (int i = 0; i < NFRAG; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
-    }
-}
-
-// Online-softmax step for one 32-query block over one 32-key tile.
-//   s      : S^T accumulator of the tile (raw q.k dot products); register i
-//            holds key (i/4)*8 + hi*4 + i%4 of the tile for this lane's query
+// Online-softmax step for one 32-query block over one 64-key tile.
+//   s      : S^T accumulators of the two 32-key halves (raw q.k dot products);
+//            register i of half kb holds key kb*32 + (i/4)*8 + hi*4 + i%4 of
+//            the tile for this lane's query
 //   c      : scale * log2(e)
 //   mref   : exponent reference (log2 units), raised lazily
 //   lsum   : running fp32 sum of exp2(s*c - mref) over this lane's keys (the
 //            unrounded weights: summing the bf16-rounded ones would move LSE
 //            by up to 2^-9 when few keys dominate)
-//   p      : bf16 P^T operands of the two 16-key MFMA steps of the tile
+//   p      : bf16 P^T operands of the four 16-key MFMA steps of the tile
 //   alpha  : factor the O accumulator must be multiplied by (1 if unchanged)
 //   upd    : wave-uniform flag: some lane raised its reference
 // MASK: keys at or past Skv (only in the last tile) get weight exactly 0.
 template <bool MASK>
-__device__ __forceinline__ void softmax_block(const f32x16 &s, float c, float &mref, float &lsum,
-                                              bf16x8 (&p)[2], float &alpha, bool &upd, int key0, int Skv)
+__device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, float &mref, float &lsum,
+                                              bf16x8 (&p)[4], float &alpha, bool &upd, int key0, int Skv)
 {
     const int hi = (threadIdx.x >> 5) & 1;
-    auto valid = [&](int i) { return key0 + (i >> 2) * 8 + hi * 4 + (i & 3) < Skv; };
-    float mx = -INFINITY;
+    auto valid = [&](int kb, int i) { return key0 + kb * 32 + (i >> 2) * 8 + hi * 4 + (i & 3) < Skv; };
+    float m0 = -INFINITY, m1 = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, (!MASK || valid(i)) ? s[i] : -INFINITY);
-    const float mt = pair_max(mx) * c;
+    for (int i = 0; i < 16; ++i) {
+        m0 = fmaxf(m0, (!MASK || valid(0, i)) ? s[0][i] : -INFINITY);
+        m1 = fmaxf(m1, (!MASK || valid(1, i)) ? s[1][i] : -INFINITY);
+    }
+    const float mt = pair_max(fmaxf(m0, m1)) * c;
     upd = __builtin_amdgcn_ballot_w64(mt > mref + kRescaleThreshold) != 0;
     const float mnew = upd ? fmaxf(mref, mt) : mref;
     alpha = __builtin_amdgcn_exp2f(mref - mnew);
@@ -172,21 +147,20 @@ __device__ __forceinline__ void softmax_block(const f32x16 &s, float c, float &m
     const float nm = -mnew;
     float acc0 = 0.f, acc1 = 0.f;
 #pragma unroll
-    for (int i = 0; i < 16; i += 2) {
-        float e0 = __builtin_amdgcn_exp2f(fmaf(s[i], c, nm));
-        float e1 = __builtin_amdgcn_exp2f(fmaf(s[i + 1], c, nm));
-        if (MASK) {
-            e0 = valid(i) ? e0 : 0.f;
-            e1 = valid(i + 1) ? e1 : 0.f;
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; i += 2) {
+            float e0 = __builtin_amdgcn_exp2f(fmaf(s[kb][i], c, nm));
+            float e1 = __builtin_amdgcn_exp2f(fmaf(s[kb][i + 1], c, nm));
+            if (MASK) {
+                e0 = valid(kb, i) ? e0 : 0.f;
+                e1 = valid(kb, i + 1) ? e1 : 0.f;
+            }
+            p[kb * 2 + (i >> 3)][i & 7] = (__bf16)e0;
+            p[kb * 2 + (i >> 3)][(i & 7) + 1] = (__bf16)e1;
+            acc0 += e0;
+            acc1 += e1;
         }
-        bf16x2 pk;
-        pk[0] = (__bf16)e0;
-        pk[1] = (__bf16)e1;
-        p[i >> 3][i & 7] = pk[0];
-        p[i >> 3][(i & 7) + 1] = pk[1];
-        acc0 += e0;
-        acc1 += e1;
-    }
     lsum = fmaf(lsum, alpha, acc0 + acc1);
 }
 
@@ -197,12 +171,12 @@ __device__ __forceinline__ void wait_vmcnt()
 }
 
 template <int D, bool OUT_F32>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_kernel(AttnArgs a, int n_qtiles)
 {
     using G = Geo<D>;
     constexpr int NCH = G::NCH, DS = G::DS, DB = G::DB, LOADS = G::LOADS;
-    constexpr int BM = kWaves * 64;
+    constexpr int BM = kWaves * 32;
     constexpr int PER_TILE = 2 * LOADS;  // copies in flight per thread per tile (K and V)
 
     __shared__ __attribute__((aligned(1024))) char smem[G::LDS];
@@ -221,7 +195,7 @@ void attn_fwd_kernel(AttnArgs a, int n_qtiles)
     bid /= n_qtiles;
     const int h = bid % a.H;
     const int b = bid / a.H;
-    const int q0 = qt * BM + wave * 64;
+    const int qi = qt * BM + wave * 32 + col;  // this lane's query
 
     const uint16_t *qp = static_cast<const uint16_t *>(a.q) + b * a.q_sb + h * a.q_sh;
     const uint16_t *kp = static_cast<const uint16_t *>(a.k) + b * a.k_sb + h * a.k_sh;
@@ -231,17 +205,13 @@ void attn_fwd_kernel(AttnArgs a, int n_qtiles)
     const bool ragged = (Skv % kBlockN) != 0;
 
     // Q^T operand fragments stay in registers for the whole key loop.
-    bf16x8 qf[2][DS];
+    bf16x8 qf[DS];
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-        const int qi = q0 + qb * 32 + col;
-#pragma unroll
-        for (int ds = 0; ds < DS; ++ds) {
-            if (qi < Sq)
-                qf[qb][ds] = *reinterpret_cast<const bf16x8 *>(qp + (int64_t)qi * a.q_ss + ds * 16 + hi * 8);
-            else
-                qf[qb][ds] = bf16x8{};
-        }
+    for (int ds = 0; ds < DS; ++ds) {
+        if (qi < Sq)
+            qf[ds] = *reinterpret_cast<const bf16x8 *>(qp + (int64_t)qi * a.q_ss + ds * 16 + hi * 8);
+        else
+            qf[ds] = bf16x8{};
     }
 
     // HBM -> LDS copy of key tile `tile` (clamped to the last tile) into its
@@ -282,31 +252,30 @@ void attn_fwd_kernel(AttnArgs a, int n_qtiles)
         voff[db] = G::TILE + (row * D + v_slot<NCH>(row, dcol >> 3) * 8 + (dcol & 7)) * 2;
     }
 
-    // S^T of both query blocks from the K tile of `tile`.
+    // S^T (two 32-key halves) from the K tile of `tile`.
     auto qk = [&](int tile, f32x16 (&s)[2]) {
         const lds_char *kt = (const lds_char *)(smem + (tile % kStages) * G::STAGE);
         s[0] = s[1] = f32x16{};
 #pragma unroll
-        for (int ds = 0; ds < DS; ++ds) {
-            const bf16x8 kf = *(const lds_bf16x8 *)(kt + koff[ds]);
-            s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[0][ds], s[0], 0, 0, 0);
-            s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[1][ds], s[1], 0, 0, 0);
-        }
+        for (int ds = 0; ds < DS; ++ds)
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+                const bf16x8 kf = *(const lds_bf16x8 *)(kt + koff[ds] + kb * 32 * D * 2);
+                s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ds], s[kb], 0, 0, 0);
+            }
     };
 
-    f32x16 oacc[2][DB];
+    f32x16 oacc[DB];
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-        for (int db = 0; db < DB; ++db) oacc[qb][db] = f32x16{};
+    for (int db = 0; db < DB; ++db) oacc[db] = f32x16{};
 
-    // O^T += V^T P^T for both query blocks from the V tile of `tile`.  MFMA
-    // k-step kk covers tile keys 16kk..16kk+15; the lower half-wave supplies
-    // keys {0-3, 8-11}, the upper {4-7, 12-15} (the S^T accumulator order).
-    auto pv = [&](int tile, const bf16x8 (&p0)[2], const bf16x8 (&p1)[2]) {
+    // O^T += V^T P^T from the V tile of `tile`.  MFMA k-step kk covers tile
+    // keys 16kk..16kk+15; the lower half-wave supplies keys {0-3, 8-11}, the
+    // upper {4-7, 12-15} (the S^T accumulator order).
+    auto pv = [&](int tile, const bf16x8 (&p)[4]) {
         const lds_char *vt = (const lds_char *)(smem + (tile % kStages) * G::STAGE);
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
+        for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
                 const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
@@ -314,122 +283,92 @@ void attn_fwd_kernel(AttnArgs a, int n_qtiles)
                 const bf16x4 up = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
                     (lds_bf16x4 *)(vt + voff[db] + (kk * 16 + 8) * D * 2));
                 const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
-                oacc[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, p0[kk], oacc[0][db], 0, 0, 0);
-                oacc[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, p1[kk], oacc[1][db], 0, 0, 0);
+                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, p[kk], oacc[db], 0, 0, 0);
             }
     };
 
     const float c = a.scale * kLog2e;
-    float mref[2] = {-INFINITY, -INFINITY};
-    float lsum[2] = {0.f, 0.f};
-    f32x16 scur1, snext[2];
-    bf16x8 p0cur[2], p0next[2], p1[2];
-    float alpha0 = 1.f, alpha1 = 1.f;
-    bool upd0 = false, upd1 = false;
+    float mref = -INFINITY;
+    float lsum = 0.f;
+    f32x16 scur[2], snext[2];
+    bf16x8 p[4];
+    float alpha = 1.f;
+    bool upd = false;
 
-    // Prologue: kAhead tiles in flight; S_0 and the softmax of its block 0.
+    // Prologue: kAhead tiles in flight; S_0.
 #pragma unroll
     for (int i = 0; i < kAhead; ++i) issue_loads(i);
     wait_vmcnt<(kAhead - 1) * PER_TILE>();
     __syncthreads();
-    {
-        f32x16 s0[2];
-        qk(0, s0);
-        if (nt == 1 && ragged)
-            softmax_block<true>(s0[0], c, mref[0], lsum[0], p0cur, alpha0, upd0, 0, Skv);
-        else
-            softmax_block<false>(s0[0], c, mref[0], lsum[0], p0cur, alpha0, upd0, 0, Skv);
-        scur1 = s0[1];
-    }
-    upd0 = false;  // O is still zero: nothing to rescale
+    qk(0, scur);
 
     // One tile of the pipeline.  HAS_NEXT: tile t+1 exists (S_{t+1} is
-    // computed here); MASK_NEXT / MASK_CUR: tile t+1 / t is the ragged last one.
-    auto step = [&](int t, auto has_next, auto mask_next, auto mask_cur) {
+    // computed here); MASK: tile t is the ragged last one.
+    auto step = [&](int t, auto has_next, auto mask) {
         constexpr bool HAS_NEXT = decltype(has_next)::value;
-        constexpr bool MASK_NEXT = decltype(mask_next)::value;
-        constexpr bool MASK_CUR = decltype(mask_cur)::value;
+        constexpr bool MASK = decltype(mask)::value;
         // ---- phase X
         if constexpr (HAS_NEXT) {
-            wait_vmcnt<(kAhead - 2) * PER_TILE>();  // this wave's copies of tile t+1 landed
+            wait_vmcnt<(kAhead - 1) * PER_TILE>();  // this wave's copies of tile t+1 landed
             __syncthreads();                         // ... and every other wave's
-            issue_loads(t + kAhead);                 // into the stage tile t-1 used
+            issue_loads(t + 1 + kAhead - 1);         // into the stage tile t-1 used
             qk(t + 1, snext);
         }
-        softmax_block<MASK_CUR>(scur1, c, mref[1], lsum[1], p1, alpha1, upd1, t * kBlockN, Skv);
-        if constexpr (HAS_NEXT) {
-            sched_phase_x<DS / 2>();
-            // keep the block-1 softmax in this phase (not sunk next to its use)
-            __asm__ volatile("" : : "v"(p1[0]), "v"(p1[1]), "v"(lsum[1]));
-        }
-        // ---- deferred O rescale (rare): between the two MFMA streams
-        if (upd0 || upd1) {
+        softmax_block<MASK>(scur, c, mref, lsum, p, alpha, upd, t * kBlockN, Skv);
+        // ---- O rescale (rare), outside the MFMA streams
+        if (upd) {
 #pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                oacc[0][db] *= (upd0 ? alpha0 : 1.f);
-                oacc[1][db] *= (upd1 ? alpha1 : 1.f);
-            }
+            for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
         }
-        upd0 = false;
         // ---- phase Y
-        pv(t, p0cur, p1);
+        pv(t, p);
         if constexpr (HAS_NEXT) {
-            softmax_block<MASK_NEXT>(snext[0], c, mref[0], lsum[0], p0next, alpha0, upd0, (t + 1) * kBlockN, Skv);
-            scur1 = snext[1];
-            p0cur[0] = p0next[0];
-            p0cur[1] = p0next[1];
-            sched_phase_y<DB>();
+            scur[0] = snext[0];
+            scur[1] = snext[1];
         }
     };
 
     using T_ = std::true_type;
     using F_ = std::false_type;
-    const int n_plain = ragged ? nt - 2 : nt - 1;  // tiles with a successor and no masking anywhere
-    for (int t = 0; t < n_plain; ++t) step(t, T_{}, F_{}, F_{});
-    if (ragged) {
-        if (nt >= 2) step(nt - 2, T_{}, T_{}, F_{});
-        step(nt - 1, F_{}, F_{}, T_{});
-    } else {
-        step(nt - 1, F_{}, F_{}, F_{});
-    }
+    for (int t = 0; t < nt - 1; ++t) step(t, T_{}, F_{});
+    if (ragged)
+        step(nt - 1, F_{}, T_{});
+    else
+        step(nt - 1, F_{}, F_{});
     wait_vmcnt<0>();  // the clamped trailing copies must land before the workgroup exits
 
     // Epilogue: O = O^T / l, LSE = ln2 * (m_ref + log2 l).
+    const float lt = pair_sum(lsum);
+    const float inv = 1.0f / lt;
+    if (qi < Sq) {
+        char *orow = static_cast<char *>(a.o) +
+                     ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-        const float lt = pair_sum(lsum[qb]);
-        const float inv = 1.0f / lt;
-        const int qi = q0 + qb * 32 + col;
-        if (qi < Sq) {
-            char *orow = static_cast<char *>(a.o) +
-                         ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
-            for (int db = 0; db < DB; ++db)
+            for (int gq = 0; gq < 4; ++gq) {
+                const int d = db * 32 + gq * 8 + hi * 4;
+                if constexpr (OUT_F32) {
+                    f32x4 w;
 #pragma unroll
-                for (int gq = 0; gq < 4; ++gq) {
-                    const int d = db * 32 + gq * 8 + hi * 4;
-                    if constexpr (OUT_F32) {
-                        f32x4 w;
+                    for (int e = 0; e < 4; ++e) w[e] = oacc[db][gq * 4 + e] * inv;
+                    *reinterpret_cast<f32x4 *>(orow + d * 4) = w;
+                } else {
+                    bf16x4 w;
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) w[e] = oacc[qb][db][gq * 4 + e] * inv;
-                        *reinterpret_cast<f32x4 *>(orow + d * 4) = w;
-                    } else {
-                        bf16x4 w;
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) w[e] = (__bf16)(oacc[qb][db][gq * 4 + e] * inv);
-                        *reinterpret_cast<bf16x4 *>(orow + d * 2) = w;
-                    }
+                    for (int e = 0; e < 4; ++e) w[e] = (__bf16)(oacc[db][gq * 4 + e] * inv);
+                    *reinterpret_cast<bf16x4 *>(orow + d * 2) = w;
                 }
-            if (a.lse != nullptr && hi == 0)
-                a.lse[((int64_t)b * a.H + h) * Sq + qi] = (mref[qb] + __log2f(lt)) * kLn2;
-        }
+            }
+        if (a.lse != nullptr && hi == 0)
+            a.lse[((int64_t)b * a.H + h) * Sq + qi] = (mref + __log2f(lt)) * kLn2;
     }
 }
 
 template <int D, bool OUT_F32>
 hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream)
 {
-    constexpr int BM = kWaves * 64;
+    constexpr int BM = kWaves * 32;
     const int n_qtiles = (a.Sq + BM - 1) / BM;
     const int64_t nblocks = (int64_t)n_qtiles * a.H * a.B;
     if (nblocks > 0x7fffffff) return hipErrorInvalidConfiguration;
