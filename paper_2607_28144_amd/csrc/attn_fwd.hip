@@ -45,6 +45,9 @@
 
 #include <math.h>
 
+#include <atomic>
+#include <cstdint>
+#include <mutex>
 #include <type_traits>
 
 namespace regenvc {
@@ -172,7 +175,7 @@ __device__ __forceinline__ void wait_vmcnt()
 
 template <int D, bool OUT_F32>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void attn_fwd_kernel(AttnArgs a, int n_qtiles)
+void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 {
     using G = Geo<D>;
     constexpr int NCH = G::NCH, DS = G::DS, DB = G::DB, LOADS = G::LOADS;
@@ -186,23 +189,39 @@ void attn_fwd_kernel(AttnArgs a, int n_qtiles)
     const int hi = lane >> 5;   // which half of the wave
     const int col = lane & 31;  // query column owned in the 32x32 accumulators
 
-    // XCD-aware renumbering: workgroup i runs on XCD i % 8; give each XCD a
-    // contiguous range of (b, h, q-tile) so one head's tiles share an L2.
-    const int nwg = gridDim.x;
-    const int xcd = blockIdx.x & 7;
-    int bid = xcd * (nwg >> 3) + min(xcd, nwg & 7) + (blockIdx.x >> 3);
-    const int qt = bid % n_qtiles;
-    bid /= n_qtiles;
-    const int h = bid % a.H;
-    const int b = bid / a.H;
-    const int qi = qt * BM + wave * 32 + col;  // this lane's query
+    // Work item of this workgroup: a whole query tile (data-parallel part) or
+    // one key range of a split tile.  Whole tiles are renumbered XCD-aware:
+    // workgroup i runs on XCD i % 8, and each XCD gets a contiguous range of
+    // tiles so that one head's tiles share an L2.
+    int tile, kt0, kt1, slot;
+    const int item = blockIdx.x;
+    if (item < pl.n_dp) {
+        const int xcd = item & 7;
+        tile = xcd * (pl.n_dp >> 3) + min(xcd, pl.n_dp & 7) + (item >> 3);
+        kt0 = 0;
+        kt1 = pl.n_kt;
+        slot = -1;
+    } else {
+        const int u = item - pl.n_dp;
+        const int sgi = u % pl.seg;
+        tile = pl.n_dp + u / pl.seg;
+        kt0 = (int)((int64_t)sgi * pl.n_kt / pl.seg);
+        kt1 = (int)((int64_t)(sgi + 1) * pl.n_kt / pl.seg);
+        slot = u;
+    }
+    const int qt = tile % pl.n_qtiles;
+    const int bh = tile / pl.n_qtiles;
+    const int h = bh % a.H;
+    const int b = bh / a.H;
+    const int qrow = wave * 32 + col;  // this lane's query within the tile
+    const int qi = qt * BM + qrow;     // ... and in the sequence
 
     const uint16_t *qp = static_cast<const uint16_t *>(a.q) + b * a.q_sb + h * a.q_sh;
     const uint16_t *kp = static_cast<const uint16_t *>(a.k) + b * a.k_sb + h * a.k_sh;
     const uint16_t *vp = static_cast<const uint16_t *>(a.v) + b * a.v_sb + h * a.v_sh;
     const int Sq = a.Sq, Skv = a.Skv;
-    const int nt = (Skv + kBlockN - 1) / kBlockN;
-    const bool ragged = (Skv % kBlockN) != 0;
+    // only the last key tile of the whole sequence can be ragged
+    const bool ragged_end = kt1 == pl.n_kt && (Skv % kBlockN) != 0;
 
     // Q^T operand fragments stay in registers for the whole key loop.
     bf16x8 qf[DS];
@@ -221,7 +240,7 @@ void attn_fwd_kernel(AttnArgs a, int n_qtiles)
     // weight is 0).  Every call issues exactly PER_TILE copies per thread, so
     // the vmcnt waits below count whole tiles.
     auto issue_loads = [&](int tile) {
-        tile = min(tile, nt - 1);
+        tile = min(tile, kt1 - 1);
         const uint32_t kdst = (uint32_t)(uintptr_t)(lds_char *)(smem + (tile % kStages) * G::STAGE);
         const uint32_t vdst = kdst + G::TILE;
         const int key0 = tile * kBlockN;
@@ -295,12 +314,12 @@ void attn_fwd_kernel(AttnArgs a, int n_qtiles)
     float alpha = 1.f;
     bool upd = false;
 
-    // Prologue: kAhead tiles in flight; S_0.
+    // Prologue: kAhead tiles in flight; S of the first tile.
 #pragma unroll
-    for (int i = 0; i < kAhead; ++i) issue_loads(i);
+    for (int i = 0; i < kAhead; ++i) issue_loads(kt0 + i);
     wait_vmcnt<(kAhead - 1) * PER_TILE>();
     __syncthreads();
-    qk(0, scur);
+    qk(kt0, scur);
 
     // One tile of the pipeline.  HAS_NEXT: tile t+1 exists (S_{t+1} is
     // computed here); MASK: tile t is the ragged last one.
@@ -309,7 +328,9 @@ void attn_fwd_kernel(AttnArgs a, int n_qtiles)
         constexpr bool MASK = decltype(mask)::value;
         // ---- phase X
         if constexpr (HAS_NEXT) {
-            wait_vmcnt<(kAhead - 1) * PER_TILE>();  // this wave's copies of tile t+1 landed
+            // tiles up to t + kAhead - 1 have been issued; tile t+1 must have
+            // landed, so at most kAhead - 2 tiles' copies may still be in flight
+            wait_vmcnt<(kAhead - 2) * PER_TILE>();  // this wave's copies of tile t+1 landed
             __syncthreads();                         // ... and every other wave's
             issue_loads(t + 1 + kAhead - 1);         // into the stage tile t-1 used
             qk(t + 1, snext);
@@ -330,51 +351,201 @@ void attn_fwd_kernel(AttnArgs a, int n_qtiles)
 
     using T_ = std::true_type;
     using F_ = std::false_type;
-    for (int t = 0; t < nt - 1; ++t) step(t, T_{}, F_{});
-    if (ragged)
-        step(nt - 1, F_{}, T_{});
+    for (int t = kt0; t < kt1 - 1; ++t) step(t, T_{}, F_{});
+    if (ragged_end)
+        step(kt1 - 1, F_{}, T_{});
     else
-        step(nt - 1, F_{}, F_{});
+        step(kt1 - 1, F_{}, F_{});
     wait_vmcnt<0>();  // the clamped trailing copies must land before the workgroup exits
 
-    // Epilogue: O = O^T / l, LSE = ln2 * (m_ref + log2 l).
+    // Epilogue: O = O^T / l, LSE = ln2 * (m_ref + log2 l); a split tile's
+    // unit writes its normalized partial to the workspace instead.
     const float lt = pair_sum(lsum);
     const float inv = 1.0f / lt;
+    const float lse_val = (mref + __log2f(lt)) * kLn2;
     if (qi < Sq) {
-        char *orow = static_cast<char *>(a.o) +
-                     ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
+        if (slot >= 0) {
+            float *orow = pl.ws_o + ((int64_t)slot * BM + qrow) * D;
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
+            for (int db = 0; db < DB; ++db)
 #pragma unroll
-            for (int gq = 0; gq < 4; ++gq) {
-                const int d = db * 32 + gq * 8 + hi * 4;
-                if constexpr (OUT_F32) {
+                for (int gq = 0; gq < 4; ++gq) {
                     f32x4 w;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) w[e] = oacc[db][gq * 4 + e] * inv;
-                    *reinterpret_cast<f32x4 *>(orow + d * 4) = w;
-                } else {
-                    bf16x4 w;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) w[e] = (__bf16)(oacc[db][gq * 4 + e] * inv);
-                    *reinterpret_cast<bf16x4 *>(orow + d * 2) = w;
+                    *reinterpret_cast<f32x4 *>(orow + db * 32 + gq * 8 + hi * 4) = w;
                 }
-            }
-        if (a.lse != nullptr && hi == 0)
-            a.lse[((int64_t)b * a.H + h) * Sq + qi] = (mref + __log2f(lt)) * kLn2;
+            if (hi == 0) pl.ws_lse[(int64_t)slot * BM + qrow] = lse_val;
+        } else {
+            char *orow = static_cast<char *>(a.o) +
+                         ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+                for (int gq = 0; gq < 4; ++gq) {
+                    const int d = db * 32 + gq * 8 + hi * 4;
+                    if constexpr (OUT_F32) {
+                        f32x4 w;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) w[e] = oacc[db][gq * 4 + e] * inv;
+                        *reinterpret_cast<f32x4 *>(orow + d * 4) = w;
+                    } else {
+                        bf16x4 w;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) w[e] = (__bf16)(oacc[db][gq * 4 + e] * inv);
+                        *reinterpret_cast<bf16x4 *>(orow + d * 2) = w;
+                    }
+                }
+            if (a.lse != nullptr && hi == 0) a.lse[((int64_t)b * a.H + h) * Sq + qi] = lse_val;
+        }
     }
+}
+
+// Log-sum-exp combination of the key-range partials of each split tile
+// (the same identity as the chunk merge): one thread per 4 dims of one row.
+template <bool OUT_F32>
+__global__ __launch_bounds__(256) void split_fixup_kernel(AttnArgs a, AttnPlan pl)
+{
+    constexpr int BM = kWaves * 32;
+    const int per_row = a.D / 4;
+    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t rows = (int64_t)(pl.n_tiles - pl.n_dp) * BM;
+    const int64_t row = gid / per_row;
+    if (row >= rows) return;
+    const int d = (int)(gid % per_row) * 4;
+    const int j = (int)(row / BM), r = (int)(row % BM);
+    const int tile = pl.n_dp + j;
+    const int qt = tile % pl.n_qtiles;
+    const int bh = tile / pl.n_qtiles;
+    const int h = bh % a.H, b = bh / a.H;
+    const int qi = qt * BM + r;
+    if (qi >= a.Sq) return;
+    const int64_t u0 = (int64_t)j * pl.seg;
+    float m = -INFINITY;
+    for (int c = 0; c < pl.seg; ++c) m = fmaxf(m, pl.ws_lse[(u0 + c) * BM + r]);
+    float s = 0.f;
+    for (int c = 0; c < pl.seg; ++c) s += expf(pl.ws_lse[(u0 + c) * BM + r] - m);
+    const float L = m + logf(s);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < pl.seg; ++c) {
+        const float w = expf(pl.ws_lse[(u0 + c) * BM + r] - L);
+        acc += w * *reinterpret_cast<const f32x4 *>(pl.ws_o + ((u0 + c) * BM + r) * a.D + d);
+    }
+    char *orow = static_cast<char *>(a.o) +
+                 ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
+    if constexpr (OUT_F32) {
+        *reinterpret_cast<f32x4 *>(orow + d * 4) = acc;
+    } else {
+        bf16x4 w;
+        for (int e = 0; e < 4; ++e) w[e] = (__bf16)acc[e];
+        *reinterpret_cast<bf16x4 *>(orow + d * 2) = w;
+    }
+    if (a.lse != nullptr && d == 0) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = L;
+}
+
+// Chooses the work plan by a cost model in units of one key-tile iteration
+// of one workgroup: whole tiles cost n_kt + 1 (prologue and epilogue), a
+// split unit costs its key range + 1.5 (the partial store), and the partials'
+// write + read traffic is priced at 5 TB/s against ~1 us per iteration.
+AttnPlan make_plan(int n_qtiles, int n_tiles, int n_kt, int n_cu, int D)
+{
+    constexpr int BM = kWaves * 32;
+    AttnPlan pl{};
+    pl.n_qtiles = n_qtiles;
+    pl.n_tiles = n_tiles;
+    pl.n_kt = n_kt;
+    pl.n_dp = n_tiles;
+    pl.seg = 1;
+    pl.n_units = 0;
+    const double whole = n_kt + 1.0;
+    double best = (double)((n_tiles + n_cu - 1) / n_cu) * whole;
+    const int rounds = n_tiles / n_cu;
+    const int rem = n_tiles - rounds * n_cu;
+    if (rem == 0 || n_kt < 2) return pl;
+    for (int seg = 2; seg <= n_kt && seg <= 256; ++seg) {
+        const int64_t units = (int64_t)rem * seg;
+        if (units > 0x7fffffff - (int64_t)n_tiles) break;
+        const int64_t sk_rounds = (units + n_cu - 1) / n_cu;
+        const int len = (n_kt + seg - 1) / seg;
+        const double traffic = 2.0 * units * BM * (D + 1) * 4 / 5e12 / 1e-6;
+        const double cost = rounds * whole + sk_rounds * (len + 1.5) + traffic;
+        if (cost < best) {
+            best = cost;
+            pl.n_dp = rounds * n_cu;
+            pl.seg = seg;
+            pl.n_units = (int)units;
+        }
+    }
+    return pl;
+}
+
+int cu_count()
+{
+    static std::atomic<int> cached[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 256;
+    if (dev >= 0 && dev < 64 && cached[dev].load() > 0) return cached[dev].load();
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    if (dev >= 0 && dev < 64) cached[dev].store(n);
+    return n;
+}
+
+// Stream-ordered workspace for split-tile partials, from a per-device pool
+// that keeps its memory (so steady-state calls do not go back to the driver).
+hipMemPool_t workspace_pool()
+{
+    static std::mutex mu;
+    static hipMemPool_t pools[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+    std::lock_guard<std::mutex> lock(mu);
+    if (pools[dev] == nullptr) {
+        hipMemPoolProps props{};
+        props.allocType = hipMemAllocationTypePinned;
+        props.location.type = hipMemLocationTypeDevice;
+        props.location.id = dev;
+        hipMemPool_t p = nullptr;
+        if (hipMemPoolCreate(&p, &props) != hipSuccess) return nullptr;
+        uint64_t keep = UINT64_MAX;
+        hipMemPoolSetAttribute(p, hipMemPoolAttrReleaseThreshold, &keep);
+        pools[dev] = p;
+    }
+    return pools[dev];
 }
 
 template <int D, bool OUT_F32>
 hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream)
 {
     constexpr int BM = kWaves * 32;
-    const int n_qtiles = (a.Sq + BM - 1) / BM;
-    const int64_t nblocks = (int64_t)n_qtiles * a.H * a.B;
-    if (nblocks > 0x7fffffff) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((attn_fwd_kernel<D, OUT_F32>), dim3((unsigned)nblocks), dim3(kThreads), 0, stream, a,
-                       n_qtiles);
-    return hipGetLastError();
+    const int64_t n_qtiles = (a.Sq + BM - 1) / BM;
+    const int64_t n_tiles = n_qtiles * a.H * a.B;
+    if (n_tiles > 0x7fffffff) return hipErrorInvalidConfiguration;
+    const int n_kt = (a.Skv + kBlockN - 1) / kBlockN;
+    AttnPlan pl = make_plan((int)n_qtiles, (int)n_tiles, n_kt, cu_count(), D);
+    void *ws = nullptr;
+    if (pl.n_units > 0) {
+        const size_t bytes = (size_t)pl.n_units * BM * (D + 1) * sizeof(float);
+        hipMemPool_t pool = workspace_pool();
+        hipError_t e = pool ? hipMallocFromPoolAsync(&ws, bytes, pool, stream) : hipErrorOutOfMemory;
+        if (e != hipSuccess) return e;
+        pl.ws_o = static_cast<float *>(ws);
+        pl.ws_lse = pl.ws_o + (size_t)pl.n_units * BM * D;
+    }
+    hipLaunchKernelGGL((attn_fwd_kernel<D, OUT_F32>), dim3((unsigned)(pl.n_dp + pl.n_units)), dim3(kThreads), 0,
+                       stream, a, pl);
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess && pl.n_units > 0) {
+        const int64_t threads = (int64_t)(pl.n_tiles - pl.n_dp) * BM * (D / 4);
+        hipLaunchKernelGGL(split_fixup_kernel<OUT_F32>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
+                           stream, a, pl);
+        e = hipGetLastError();
+    }
+    if (ws != nullptr) {
+        const hipError_t ef = hipFreeAsync(ws, stream);
+        if (e == hipSuccess) e = ef;
+    }
+    return e;
 }
 
 }  // namespace

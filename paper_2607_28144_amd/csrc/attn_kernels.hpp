@@ -20,6 +20,23 @@ struct AttnArgs {
     float scale;
 };
 
+// Work plan of one attention launch.  Query tiles [0, n_dp) are processed
+// whole, one workgroup each (data-parallel rounds); tiles [n_dp, n_tiles) are
+// each split into `seg` contiguous key ranges ("units", one workgroup each)
+// whose normalized partial O and LSE go to a workspace and are combined by a
+// log-sum-exp fixup.  Splitting only the leftover tiles keeps every CU busy
+// when the tile count is just above a multiple of the CU count.
+struct AttnPlan {
+    int32_t n_qtiles;  // query tiles per (batch, head)
+    int32_t n_tiles;   // B * H * n_qtiles
+    int32_t n_kt;      // key tiles per query tile
+    int32_t n_dp;      // tiles processed whole
+    int32_t seg;       // key ranges per split tile (>= 2 when n_units > 0)
+    int32_t n_units;   // (n_tiles - n_dp) * seg
+    float *ws_o;       // [n_units][query tile rows][D] partial O (normalized)
+    float *ws_lse;     // [n_units][query tile rows] partial LSE
+};
+
 struct MergeArgs {
     const float *o_parts[16];
     const float *lse_parts[16];
