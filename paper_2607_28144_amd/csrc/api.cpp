@@ -224,6 +224,7 @@ regenvc_status attn_common(const char *fn, const regenvc_tensor *q, const regenv
     a.D = D;
     a.o_f32 = o_dtype == REGENVC_F32;
     a.scale = scale;
+    a.kv_off32 = k->stride_s >= 0 && v->stride_s >= 0 && k->stride_s < (1 << 24) && v->stride_s < (1 << 24);
     return launched(regenvc::launch_attn(a, static_cast<hipStream_t>(stream)), fn);
 }
 

@@ -105,6 +105,22 @@ __device__ __forceinline__ void lds_dma16(const void *gptr, uint32_t lds_base)
     __asm__ volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" : : "s"(base), "v"(gptr) : "m0");
 }
 
+// Same copy with a scalar (wave-uniform) base address and a 32-bit lane offset.
+__device__ __forceinline__ void lds_dma16_s(const void *gbase, uint32_t off, uint32_t lds_base)
+{
+    const uint32_t base = __builtin_amdgcn_readfirstlane(lds_base);
+    const uint64_t g = (uint64_t)(uintptr_t)gbase;
+    // readfirstlane yields an int: widen each half through uint32_t so the low
+    // half is zero-extended (a sign-extended low half corrupts the address)
+    const uint32_t ghi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(g >> 32));
+    const uint32_t glo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)g);
+    const uint64_t gs = ((uint64_t)ghi << 32) | (uint64_t)glo;
+    __asm__ volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                     :
+                     : "s"(base), "v"(off), "s"((const void *)(uintptr_t)gs)
+                     : "m0");
+}
+
 // (x of this lane, x of lane^32) combined so both halves hold the same value.
 __device__ __forceinline__ float pair_max(float x)
 {
@@ -185,7 +201,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     __shared__ __attribute__((aligned(1024))) char smem[G::LDS];
 
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
     const int hi = lane >> 5;   // which half of the wave
     const int col = lane & 31;  // query column owned in the 32x32 accumulators
 
@@ -233,28 +249,47 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
             qf[ds] = bf16x8{};
     }
 
-    // HBM -> LDS copy of key tile `tile` (clamped to the last tile) into its
+    // HBM -> LDS copy of key tile `tl` (clamped to the last tile) into its
     // ring stage.  Each wave instruction fills 1 KB of LDS (64 lanes x 16 B,
     // in lane order); the lane fetches the chunk the swizzle places there.
     // Rows past the last key re-read the last key (finite data; their softmax
     // weight is 0).  Every call issues exactly PER_TILE copies per thread, so
     // the vmcnt waits below count whole tiles.
-    auto issue_loads = [&](int tile) {
-        tile = min(tile, kt1 - 1);
-        const uint32_t kdst = (uint32_t)(uintptr_t)(lds_char *)(smem + (tile % kStages) * G::STAGE);
-        const uint32_t vdst = kdst + G::TILE;
-        const int key0 = tile * kBlockN;
-        const int last = Skv - 1 - key0;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char *)smem;
+    uint32_t kofs[LOADS], vofs[LOADS];
 #pragma unroll
-        for (int j = 0; j < LOADS; ++j) {
-            const int blk = wave * LOADS + j;
-            const int slot = blk * 64 + lane;
-            const int row = slot / NCH, phys = slot % NCH;
-            const int64_t key = key0 + min(row, last);
-            const uint16_t *gk = kp + key * a.k_ss + k_slot<NCH>(row, phys) * 8;
-            const uint16_t *gv = vp + key * a.v_ss + v_slot<NCH>(row, phys) * 8;
-            lds_dma16(gk, kdst + blk * 1024);
-            lds_dma16(gv, vdst + blk * 1024);
+    for (int j = 0; j < LOADS; ++j) {
+        const int slot16 = (wave * LOADS + j) * 64 + lane;
+        const int row = slot16 / NCH, phys = slot16 % NCH;
+        kofs[j] = (uint32_t)((row * a.k_ss + k_slot<NCH>(row, phys) * 8) * 2);
+        vofs[j] = (uint32_t)((row * a.v_ss + v_slot<NCH>(row, phys) * 8) * 2);
+    }
+    auto issue_loads = [&](int tl) {
+        tl = min(tl, kt1 - 1);
+        const uint32_t kdst = lds0 + (tl % kStages) * G::STAGE;
+        const uint32_t vdst = kdst + G::TILE;
+        const int key0 = tl * kBlockN;
+        if (a.kv_off32 && key0 + kBlockN <= Skv) {
+            // full tile: scalar tile base + precomputed 32-bit lane offsets
+            const uint16_t *kb = kp + (int64_t)key0 * a.k_ss;
+            const uint16_t *vb = vp + (int64_t)key0 * a.v_ss;
+#pragma unroll
+            for (int j = 0; j < LOADS; ++j) {
+                const uint32_t blk = (wave * LOADS + j) * 1024;
+                lds_dma16_s(kb, kofs[j], kdst + blk);
+                lds_dma16_s(vb, vofs[j], vdst + blk);
+            }
+        } else {
+            const int last = Skv - 1 - key0;
+#pragma unroll
+            for (int j = 0; j < LOADS; ++j) {
+                const int blk = wave * LOADS + j;
+                const int slot16 = blk * 64 + lane;
+                const int row = slot16 / NCH, phys = slot16 % NCH;
+                const int64_t key = key0 + min(row, last);
+                lds_dma16(kp + key * a.k_ss + k_slot<NCH>(row, phys) * 8, kdst + blk * 1024);
+                lds_dma16(vp + key * a.v_ss + v_slot<NCH>(row, phys) * 8, vdst + blk * 1024);
+            }
         }
     };
 

@@ -18,6 +18,9 @@ struct AttnArgs {
     int32_t B, H, Sq, Skv, D;
     bool o_f32;
     float scale;
+    // K/V row offsets within a 64-key tile fit 31 bits (non-negative strides
+    // below 2^24 elements): tile copies use a scalar base + 32-bit lane offsets
+    bool kv_off32;
 };
 
 // Work plan of one attention launch.  Query tiles [0, n_dp) are processed
