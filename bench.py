@@ -100,8 +100,8 @@ def copy_reference(torch, dev, args):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=20, help="untimed steps (the clock settles under load)")
     ap.add_argument("--only", choices=["self", "cross", "share", "copy"], default=None,
                     help="time one component alone (for profiling); 'copy' runs a plain 1 GiB elementwise "
                          "copy kernel, the reference for scaling HBM byte counters")

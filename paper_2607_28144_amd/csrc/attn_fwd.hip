@@ -306,39 +306,54 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         voff[db] = G::TILE + (row * D + v_slot<NCH>(row, dcol >> 3) * 8 + (dcol & 7)) * 2;
     }
 
-    // S^T (two 32-key halves) from the K tile of `tile`.
-    auto qk = [&](int tile, f32x16 (&s)[2]) {
-        const lds_char *kt = (const lds_char *)(smem + (tile % kStages) * G::STAGE);
+    constexpr int NK = 2 * DS;  // K fragments (MFMAs) per tile for S^T
+    constexpr int NV = 4 * DB;  // V fragments (MFMAs) per tile for O^T
+    constexpr int PF = 4;       // fragments read ahead of their MFMA
+    static_assert(NK >= 8 && NV >= PF, "schedule assumes d >= 64");
+
+    // K fragment i (i = 2*ds + kb): rows kb*32.., dims 16*ds.. of the tile.
+    auto kfrag = [&](const lds_char *kt, int i) -> bf16x8 {
+        return *(const lds_bf16x8 *)(kt + koff[i >> 1] + (i & 1) * 32 * D * 2);
+    };
+    // V^T fragment i (i = kk*DB + db): dims 32*db.., keys 16*kk.. of the tile;
+    // the lower half-wave supplies keys {0-3, 8-11}, the upper {4-7, 12-15}
+    // (the S^T accumulator order).
+    auto vfrag = [&](const lds_char *vt, int i) -> bf16x8 {
+        const int kk = i / DB, db = i % DB;
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(vt + voff[db] + kk * 16 * D * 2));
+        const bf16x4 up =
+            __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(vt + voff[db] + (kk * 16 + 8) * D * 2));
+        return bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
+    };
+    auto stage_ptr = [&](int tl) { return (const lds_char *)(smem + (tl % kStages) * G::STAGE); };
+
+    // S^T (two 32-key halves) of key tile `tl`, plain (prologue only).
+    auto qk = [&](int tl, f32x16 (&s)[2]) {
+        const lds_char *kt = stage_ptr(tl);
         s[0] = s[1] = f32x16{};
 #pragma unroll
-        for (int ds = 0; ds < DS; ++ds)
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                const bf16x8 kf = *(const lds_bf16x8 *)(kt + koff[ds] + kb * 32 * D * 2);
-                s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ds], s[kb], 0, 0, 0);
-            }
+        for (int i = 0; i < NK; ++i)
+            s[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kfrag(kt, i), qf[i >> 1], s[i & 1], 0, 0, 0);
     };
 
     f32x16 oacc[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db) oacc[db] = f32x16{};
 
-    // O^T += V^T P^T from the V tile of `tile`.  MFMA k-step kk covers tile
-    // keys 16kk..16kk+15; the lower half-wave supplies keys {0-3, 8-11}, the
-    // upper {4-7, 12-15} (the S^T accumulator order).
-    auto pv = [&](int tile, const bf16x8 (&p)[4]) {
-        const lds_char *vt = (const lds_char *)(smem + (tile % kStages) * G::STAGE);
+    // O^T += V^T P^T for key tile `tl`: each MFMA's V fragment is read PF
+    // MFMAs ahead; the order is pinned so that the waits stay PF deep.
+    auto pv = [&](int tl, const bf16x8 (&p)[4]) {
+        const lds_char *vt = stage_ptr(tl);
+        bf16x8 vr[PF];
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
+        for (int i = 0; i < PF; ++i) vr[i] = vfrag(vt, i);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-                    (lds_bf16x4 *)(vt + voff[db] + kk * 16 * D * 2));
-                const bf16x4 up = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-                    (lds_bf16x4 *)(vt + voff[db] + (kk * 16 + 8) * D * 2));
-                const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
-                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, p[kk], oacc[db], 0, 0, 0);
-            }
+        for (int i = 0; i < NV; ++i) {
+            oacc[i % DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vr[i % PF], p[i / DB], oacc[i % DB], 0, 0, 0);
+            if (i + PF < NV) vr[i % PF] = vfrag(vt, i + PF);
+            __builtin_amdgcn_sched_barrier(0);
+        }
     };
 
     const float c = a.scale * kLog2e;
@@ -349,6 +364,60 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     float alpha = 1.f;
     bool upd = false;
 
+    // Phase X of a tile that has a successor: S_{t+1} = K_{t+1} Q^T on the
+    // MFMA pipe, and the softmax of S_t -> P_t cut into NK pieces placed one
+    // after each MFMA (max: NK/4 pieces, reference update: 1, exponentials:
+    // NK/2, row-sum update: 1), with K fragments read PF MFMAs ahead.
+    auto qk_softmax = [&](int tl_next) {
+        const lds_char *kt = stage_ptr(tl_next);
+        constexpr int MAXP = NK / 4, EXPP = NK / 2;
+        constexpr int MAXN = 32 / MAXP, EXPN = 32 / EXPP;  // values per piece
+        bf16x8 kr[PF];
+        float m0 = -INFINITY, m1 = -INFINITY, acc0 = 0.f, acc1 = 0.f, nm = 0.f;
+#pragma unroll
+        for (int i = 0; i < PF; ++i) kr[i] = kfrag(kt, i);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < NK; ++i) {
+            if (i < 2)
+                snext[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kr[i % PF], qf[i >> 1], f32x16{}, 0, 0, 0);
+            else
+                snext[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kr[i % PF], qf[i >> 1], snext[i & 1], 0, 0, 0);
+            if (i + PF < NK) kr[i % PF] = kfrag(kt, i + PF);
+            if (i < MAXP) {
+#pragma unroll
+                for (int e = i * MAXN; e < (i + 1) * MAXN; e += 2) {
+                    m0 = fmaxf(m0, scur[e >> 4][e & 15]);
+                    m1 = fmaxf(m1, scur[e >> 4][(e & 15) + 1]);
+                }
+            } else if (i == MAXP) {
+                const float mt = pair_max(fmaxf(m0, m1)) * c;
+                upd = __builtin_amdgcn_ballot_w64(mt > mref + kRescaleThreshold) != 0;
+                const float mnew = upd ? fmaxf(mref, mt) : mref;
+                alpha = __builtin_amdgcn_exp2f(mref - mnew);
+                mref = mnew;
+                nm = -mnew;
+            } else if (i < MAXP + 1 + EXPP) {
+                const int e0 = (i - MAXP - 1) * EXPN;
+#pragma unroll
+                for (int e = e0; e < e0 + EXPN; e += 2) {
+                    const float x0 = __builtin_amdgcn_exp2f(fmaf(scur[e >> 4][e & 15], c, nm));
+                    const float x1 = __builtin_amdgcn_exp2f(fmaf(scur[e >> 4][(e & 15) + 1], c, nm));
+                    p[e >> 3][e & 7] = (__bf16)x0;
+                    p[e >> 3][(e & 7) + 1] = (__bf16)x1;
+                    acc0 += x0;
+                    acc1 += x1;
+                }
+            } else if (i == MAXP + 1 + EXPP) {
+                lsum = fmaf(lsum, alpha, acc0 + acc1);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        // keep the softmax in this phase: without a use here the compiler
+        // sinks it past the rescale branch, next to the P V products
+        __asm__ volatile("" : : "v"(p[0]), "v"(p[1]), "v"(p[2]), "v"(p[3]), "v"(lsum));
+    };
+
     // Prologue: kAhead tiles in flight; S of the first tile.
 #pragma unroll
     for (int i = 0; i < kAhead; ++i) issue_loads(kt0 + i);
@@ -357,7 +426,8 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     qk(kt0, scur);
 
     // One tile of the pipeline.  HAS_NEXT: tile t+1 exists (S_{t+1} is
-    // computed here); MASK: tile t is the ragged last one.
+    // computed here, beside the softmax of S_t); MASK: tile t is the ragged
+    // last one.
     auto step = [&](int t, auto has_next, auto mask) {
         constexpr bool HAS_NEXT = decltype(has_next)::value;
         constexpr bool MASK = decltype(mask)::value;
@@ -368,9 +438,10 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
             wait_vmcnt<(kAhead - 2) * PER_TILE>();  // this wave's copies of tile t+1 landed
             __syncthreads();                         // ... and every other wave's
             issue_loads(t + 1 + kAhead - 1);         // into the stage tile t-1 used
-            qk(t + 1, snext);
+            qk_softmax(t + 1);
+        } else {
+            softmax_block<MASK>(scur, c, mref, lsum, p, alpha, upd, t * kBlockN, Skv);
         }
-        softmax_block<MASK>(scur, c, mref, lsum, p, alpha, upd, t * kBlockN, Skv);
         // ---- O rescale (rare), outside the MFMA streams
         if (upd) {
 #pragma unroll
