@@ -340,9 +340,25 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 #pragma unroll
     for (int db = 0; db < DB; ++db) oacc[db] = f32x16{};
 
+    const float c = a.scale * kLog2e;
+    float mref = -INFINITY;
+    float lsum = 0.f;
+    f32x16 scur[2], snext[2];
+    bf16x8 p[4];
+    float alpha = 1.f;
+    bool upd = false;
+    // softmax state carried from phase X into phase Y of a step
+    float nm = 0.f, acc0 = 0.f, acc1 = 0.f;
+
     // O^T += V^T P^T for key tile `tl`: each MFMA's V fragment is read PF
-    // MFMAs ahead; the order is pinned so that the waits stay PF deep.
-    auto pv = [&](int tl, const bf16x8 (&p)[4]) {
+    // MFMAs ahead; the order is pinned so that the waits stay PF deep.  With
+    // `tail`, the MFMAs carry the second half of the softmax of this tile
+    // (weights of S values 16..31, i.e. P operands 2 and 3): one piece after
+    // each of the first NV/2 MFMAs, so that P operand 2 is complete NV/4
+    // MFMAs before its first use and operand 3 NV/4 + 1 before its.
+    auto pv = [&](int tl, auto tail, const f32x16 (&sc)[2]) {
+        constexpr bool TAIL = decltype(tail)::value;
+        constexpr int TN = 32 / NV;  // weights per piece
         const lds_char *vt = stage_ptr(tl);
         bf16x8 vr[PF];
 #pragma unroll
@@ -352,43 +368,57 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         for (int i = 0; i < NV; ++i) {
             oacc[i % DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vr[i % PF], p[i / DB], oacc[i % DB], 0, 0, 0);
             if (i + PF < NV) vr[i % PF] = vfrag(vt, i + PF);
+            if constexpr (TAIL) {
+                if (i < NV / 2) {
+#pragma unroll
+                    for (int e = 16 + i * TN; e < 16 + (i + 1) * TN; e += 2) {
+                        const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[e >> 4][e & 15], c, nm));
+                        const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[e >> 4][(e & 15) + 1], c, nm));
+                        p[e >> 3][e & 7] = (__bf16)x0;
+                        p[e >> 3][(e & 7) + 1] = (__bf16)x1;
+                        acc0 += x0;
+                        acc1 += x1;
+                    }
+                } else if (i == NV / 2) {
+                    lsum = fmaf(lsum, alpha, acc0 + acc1);
+                }
+            }
             __builtin_amdgcn_sched_barrier(0);
         }
     };
 
-    const float c = a.scale * kLog2e;
-    float mref = -INFINITY;
-    float lsum = 0.f;
-    f32x16 scur[2], snext[2];
-    bf16x8 p[4];
-    float alpha = 1.f;
-    bool upd = false;
 
     // Phase X of a tile that has a successor: S_{t+1} = K_{t+1} Q^T on the
-    // MFMA pipe, and the softmax of S_t -> P_t cut into NK pieces placed one
-    // after each MFMA (max: NK/4 pieces, reference update: 1, exponentials:
-    // NK/2, row-sum update: 1), with K fragments read PF MFMAs ahead.
-    auto qk_softmax = [&](int tl_next) {
+    // MFMA pipe, and the first half of the softmax of S_t cut into pieces
+    // placed one after each MFMA (max: NK/4 pieces, reference update: 1,
+    // weights of S values 0..15 = P operands 0 and 1: NK/2), with K fragments
+    // read PF MFMAs ahead.  The other half runs beside the P V products.
+    auto qk_softmax = [&](int tl_next, const f32x16 (&sc)[2], f32x16 (&sn)[2]) {
         const lds_char *kt = stage_ptr(tl_next);
+        // The two waves sharing a SIMD contend for its MFMA pipe; the one in
+        // this (VALU-heavy) phase goes first, and the other's P V products
+        // fill the gaps between its MFMAs.
+        __builtin_amdgcn_s_setprio(1);
         constexpr int MAXP = NK / 4, EXPP = NK / 2;
-        constexpr int MAXN = 32 / MAXP, EXPN = 32 / EXPP;  // values per piece
+        constexpr int MAXN = 32 / MAXP, EXPN = 16 / EXPP;  // values per piece
         bf16x8 kr[PF];
-        float m0 = -INFINITY, m1 = -INFINITY, acc0 = 0.f, acc1 = 0.f, nm = 0.f;
+        float m0 = -INFINITY, m1 = -INFINITY;
+        acc0 = acc1 = 0.f;
 #pragma unroll
         for (int i = 0; i < PF; ++i) kr[i] = kfrag(kt, i);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 0; i < NK; ++i) {
             if (i < 2)
-                snext[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kr[i % PF], qf[i >> 1], f32x16{}, 0, 0, 0);
+                sn[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kr[i % PF], qf[i >> 1], f32x16{}, 0, 0, 0);
             else
-                snext[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kr[i % PF], qf[i >> 1], snext[i & 1], 0, 0, 0);
+                sn[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kr[i % PF], qf[i >> 1], sn[i & 1], 0, 0, 0);
             if (i + PF < NK) kr[i % PF] = kfrag(kt, i + PF);
             if (i < MAXP) {
 #pragma unroll
                 for (int e = i * MAXN; e < (i + 1) * MAXN; e += 2) {
-                    m0 = fmaxf(m0, scur[e >> 4][e & 15]);
-                    m1 = fmaxf(m1, scur[e >> 4][(e & 15) + 1]);
+                    m0 = fmaxf(m0, sc[e >> 4][e & 15]);
+                    m1 = fmaxf(m1, sc[e >> 4][(e & 15) + 1]);
                 }
             } else if (i == MAXP) {
                 const float mt = pair_max(fmaxf(m0, m1)) * c;
@@ -401,21 +431,19 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
                 const int e0 = (i - MAXP - 1) * EXPN;
 #pragma unroll
                 for (int e = e0; e < e0 + EXPN; e += 2) {
-                    const float x0 = __builtin_amdgcn_exp2f(fmaf(scur[e >> 4][e & 15], c, nm));
-                    const float x1 = __builtin_amdgcn_exp2f(fmaf(scur[e >> 4][(e & 15) + 1], c, nm));
+                    const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[e >> 4][e & 15], c, nm));
+                    const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[e >> 4][(e & 15) + 1], c, nm));
                     p[e >> 3][e & 7] = (__bf16)x0;
                     p[e >> 3][(e & 7) + 1] = (__bf16)x1;
                     acc0 += x0;
                     acc1 += x1;
                 }
-            } else if (i == MAXP + 1 + EXPP) {
-                lsum = fmaf(lsum, alpha, acc0 + acc1);
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        // keep the softmax in this phase: without a use here the compiler
-        // sinks it past the rescale branch, next to the P V products
-        __asm__ volatile("" : : "v"(p[0]), "v"(p[1]), "v"(p[2]), "v"(p[3]), "v"(lsum));
+        // keep this half of the softmax in this phase: without a use here the
+        // compiler sinks it past the rescale branch, next to the P V products
+        __asm__ volatile("" : : "v"(p[0]), "v"(p[1]), "v"(acc0), "v"(acc1), "v"(nm), "v"(alpha));
     };
 
     // Prologue: kAhead tiles in flight; S of the first tile.
@@ -425,10 +453,10 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     __syncthreads();
     qk(kt0, scur);
 
-    // One tile of the pipeline.  HAS_NEXT: tile t+1 exists (S_{t+1} is
-    // computed here, beside the softmax of S_t); MASK: tile t is the ragged
-    // last one.
-    auto step = [&](int t, auto has_next, auto mask) {
+    // One tile of the pipeline on the S buffers sc (S_t) and sn (S_{t+1}).
+    // HAS_NEXT: tile t+1 exists (S_{t+1} is computed here, beside the softmax
+    // of S_t); MASK: tile t is the ragged last one.
+    auto step = [&](int t, f32x16 (&sc)[2], f32x16 (&sn)[2], auto has_next, auto mask) {
         constexpr bool HAS_NEXT = decltype(has_next)::value;
         constexpr bool MASK = decltype(mask)::value;
         // ---- phase X
@@ -438,30 +466,42 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
             wait_vmcnt<(kAhead - 2) * PER_TILE>();  // this wave's copies of tile t+1 landed
             __syncthreads();                         // ... and every other wave's
             issue_loads(t + 1 + kAhead - 1);         // into the stage tile t-1 used
-            qk_softmax(t + 1);
+            qk_softmax(t + 1, sc, sn);
         } else {
-            softmax_block<MASK>(scur, c, mref, lsum, p, alpha, upd, t * kBlockN, Skv);
+            softmax_block<MASK>(sc, c, mref, lsum, p, alpha, upd, t * kBlockN, Skv);
         }
         // ---- O rescale (rare), outside the MFMA streams
         if (upd) {
 #pragma unroll
             for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
         }
-        // ---- phase Y
-        pv(t, p);
-        if constexpr (HAS_NEXT) {
-            scur[0] = snext[0];
-            scur[1] = snext[1];
-        }
+        // ---- phase Y, at normal priority (phase X raised it)
+        __builtin_amdgcn_s_setprio(0);
+        if constexpr (HAS_NEXT)
+            pv(t, std::true_type{}, sc);
+        else
+            pv(t, std::false_type{}, sc);
     };
 
     using T_ = std::true_type;
     using F_ = std::false_type;
-    for (int t = kt0; t < kt1 - 1; ++t) step(t, T_{}, F_{});
+    // Two tiles per trip with the roles of the S buffers swapped in the
+    // second, so that S_{t+1} is never copied.
+    int t = kt0;
+    for (; t + 2 < kt1; t += 2) {
+        step(t, scur, snext, T_{}, F_{});
+        step(t + 1, snext, scur, T_{}, F_{});
+    }
+    if (t + 1 < kt1) {  // two tiles left: one more step with a successor
+        step(t, scur, snext, T_{}, F_{});
+        scur[0] = snext[0];
+        scur[1] = snext[1];
+        ++t;
+    }
     if (ragged_end)
-        step(kt1 - 1, F_{}, T_{});
+        step(t, scur, snext, F_{}, T_{});
     else
-        step(kt1 - 1, F_{}, F_{});
+        step(t, scur, snext, F_{}, F_{});
     wait_vmcnt<0>();  // the clamped trailing copies must land before the workgroup exits
 
     // Epilogue: O = O^T / l, LSE = ln2 * (m_ref + log2 l); a split tile's
