@@ -249,12 +249,13 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
             qf[ds] = bf16x8{};
     }
 
-    // HBM -> LDS copy of key tile `tl` (clamped to the last tile) into its
-    // ring stage.  Each wave instruction fills 1 KB of LDS (64 lanes x 16 B,
-    // in lane order); the lane fetches the chunk the swizzle places there.
-    // Rows past the last key re-read the last key (finite data; their softmax
-    // weight is 0).  Every call issues exactly PER_TILE copies per thread, so
-    // the vmcnt waits below count whole tiles.
+    // HBM -> LDS copy of one key tile into a ring stage.  Each wave
+    // instruction fills 1 KB of LDS (64 lanes x 16 B, in lane order); the
+    // lane fetches the chunk the swizzle places there.  Rows past the last
+    // key re-read the last key (finite data; their softmax weight is 0).
+    // Copies requested past the last tile repeat it into the otherwise unused
+    // stage, so every call issues exactly PER_TILE copies per thread and the
+    // vmcnt waits below count whole tiles.
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char *)smem;
     uint32_t kofs[LOADS], vofs[LOADS];
 #pragma unroll
@@ -264,22 +265,27 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         kofs[j] = (uint32_t)((row * a.k_ss + k_slot<NCH>(row, phys) * 8) * 2);
         vofs[j] = (uint32_t)((row * a.v_ss + v_slot<NCH>(row, phys) * 8) * 2);
     }
-    auto issue_loads = [&](int tl) {
-        tl = min(tl, kt1 - 1);
-        const uint32_t kdst = lds0 + (tl % kStages) * G::STAGE;
+    // Tiles are copied in order kt0, kt0+1, ... (one call per tile); the
+    // scalar source bases advance by one tile per call and stay on the last
+    // tile once it is reached.  `stage` is the ring stage to fill.
+    const int64_t k_step = (int64_t)kBlockN * a.k_ss, v_step = (int64_t)kBlockN * a.v_ss;
+    const int last_full = Skv / kBlockN - 1;  // last tile with kBlockN keys
+    int tl_copy = kt0;
+    const uint16_t *kb_copy = kp + kt0 * k_step;
+    const uint16_t *vb_copy = vp + kt0 * v_step;
+    auto issue_next = [&](int stage) {
+        const uint32_t kdst = lds0 + stage * G::STAGE;
         const uint32_t vdst = kdst + G::TILE;
-        const int key0 = tl * kBlockN;
-        if (a.kv_off32 && key0 + kBlockN <= Skv) {
+        if (a.kv_off32 && tl_copy <= last_full) {
             // full tile: scalar tile base + precomputed 32-bit lane offsets
-            const uint16_t *kb = kp + (int64_t)key0 * a.k_ss;
-            const uint16_t *vb = vp + (int64_t)key0 * a.v_ss;
 #pragma unroll
             for (int j = 0; j < LOADS; ++j) {
                 const uint32_t blk = (wave * LOADS + j) * 1024;
-                lds_dma16_s(kb, kofs[j], kdst + blk);
-                lds_dma16_s(vb, vofs[j], vdst + blk);
+                lds_dma16_s(kb_copy, kofs[j], kdst + blk);
+                lds_dma16_s(vb_copy, vofs[j], vdst + blk);
             }
         } else {
+            const int key0 = tl_copy * kBlockN;
             const int last = Skv - 1 - key0;
 #pragma unroll
             for (int j = 0; j < LOADS; ++j) {
@@ -291,7 +297,14 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
                 lds_dma16(vp + key * a.v_ss + v_slot<NCH>(row, phys) * 8, vdst + blk * 1024);
             }
         }
+        if (tl_copy < kt1 - 1) {
+            ++tl_copy;
+            kb_copy += k_step;
+            vb_copy += v_step;
+        }
     };
+    auto next_stage = [](int st) { return st == kStages - 1 ? 0 : st + 1; };
+    static_assert(kAhead == 2 && kStages == 3, "the step issues tile t+2 into the stage of tile t-1");
 
     // Per-lane LDS byte offsets of the MFMA operand fragments (stage 0).
     int koff[DS];
@@ -325,11 +338,12 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
             __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(vt + voff[db] + (kk * 16 + 8) * D * 2));
         return bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
     };
-    auto stage_ptr = [&](int tl) { return (const lds_char *)(smem + (tl % kStages) * G::STAGE); };
+    auto stage_ptr = [&](int st) { return (const lds_char *)(smem + st * G::STAGE); };
 
-    // S^T (two 32-key halves) of key tile `tl`, plain (prologue only).
-    auto qk = [&](int tl, f32x16 (&s)[2]) {
-        const lds_char *kt = stage_ptr(tl);
+    // S^T (two 32-key halves) of the key tile in stage `st`, plain (prologue
+    // only).
+    auto qk = [&](int st, f32x16 (&s)[2]) {
+        const lds_char *kt = stage_ptr(st);
         s[0] = s[1] = f32x16{};
 #pragma unroll
         for (int i = 0; i < NK; ++i)
@@ -350,16 +364,16 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     // softmax state carried from phase X into phase Y of a step
     float nm = 0.f, acc0 = 0.f, acc1 = 0.f;
 
-    // O^T += V^T P^T for key tile `tl`: each MFMA's V fragment is read PF
+    // O^T += V^T P^T for the key tile in stage `st`: each MFMA's V fragment is read PF
     // MFMAs ahead; the order is pinned so that the waits stay PF deep.  With
     // `tail`, the MFMAs carry the second half of the softmax of this tile
     // (weights of S values 16..31, i.e. P operands 2 and 3): one piece after
     // each of the first NV/2 MFMAs, so that P operand 2 is complete NV/4
     // MFMAs before its first use and operand 3 NV/4 + 1 before its.
-    auto pv = [&](int tl, auto tail, const f32x16 (&sc)[2]) {
+    auto pv = [&](int st, auto tail, const f32x16 (&sc)[2]) {
         constexpr bool TAIL = decltype(tail)::value;
         constexpr int TN = 32 / NV;  // weights per piece
-        const lds_char *vt = stage_ptr(tl);
+        const lds_char *vt = stage_ptr(st);
         bf16x8 vr[PF];
 #pragma unroll
         for (int i = 0; i < PF; ++i) vr[i] = vfrag(vt, i);
@@ -393,8 +407,8 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     // placed one after each MFMA (max: NK/4 pieces, reference update: 1,
     // weights of S values 0..15 = P operands 0 and 1: NK/2), with K fragments
     // read PF MFMAs ahead.  The other half runs beside the P V products.
-    auto qk_softmax = [&](int tl_next, const f32x16 (&sc)[2], f32x16 (&sn)[2]) {
-        const lds_char *kt = stage_ptr(tl_next);
+    auto qk_softmax = [&](int st_next, const f32x16 (&sc)[2], f32x16 (&sn)[2]) {
+        const lds_char *kt = stage_ptr(st_next);
         // The two waves sharing a SIMD contend for its MFMA pipe; the one in
         // this (VALU-heavy) phase goes first, and the other's P V products
         // fill the gaps between its MFMAs.
@@ -447,11 +461,18 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     };
 
     // Prologue: kAhead tiles in flight; S of the first tile.
+    int st = kt0 % kStages;  // stage of tile t
+    {
+        int sl = st;
 #pragma unroll
-    for (int i = 0; i < kAhead; ++i) issue_loads(kt0 + i);
+        for (int i = 0; i < kAhead; ++i) {
+            issue_next(sl);
+            sl = next_stage(sl);
+        }
+    }
     wait_vmcnt<(kAhead - 1) * PER_TILE>();
     __syncthreads();
-    qk(kt0, scur);
+    qk(st, scur);
 
     // One tile of the pipeline on the S buffers sc (S_t) and sn (S_{t+1}).
     // HAS_NEXT: tile t+1 exists (S_{t+1} is computed here, beside the softmax
@@ -459,14 +480,15 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     auto step = [&](int t, f32x16 (&sc)[2], f32x16 (&sn)[2], auto has_next, auto mask) {
         constexpr bool HAS_NEXT = decltype(has_next)::value;
         constexpr bool MASK = decltype(mask)::value;
+        const int st1 = next_stage(st);  // stage of tile t+1
         // ---- phase X
         if constexpr (HAS_NEXT) {
             // tiles up to t + kAhead - 1 have been issued; tile t+1 must have
             // landed, so at most kAhead - 2 tiles' copies may still be in flight
             wait_vmcnt<(kAhead - 2) * PER_TILE>();  // this wave's copies of tile t+1 landed
             __syncthreads();                         // ... and every other wave's
-            issue_loads(t + 1 + kAhead - 1);         // into the stage tile t-1 used
-            qk_softmax(t + 1, sc, sn);
+            issue_next(next_stage(st1));             // tile t+kAhead, into the stage tile t-1 used
+            qk_softmax(st1, sc, sn);
         } else {
             softmax_block<MASK>(sc, c, mref, lsum, p, alpha, upd, t * kBlockN, Skv);
         }
@@ -478,9 +500,10 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         // ---- phase Y, at normal priority (phase X raised it)
         __builtin_amdgcn_s_setprio(0);
         if constexpr (HAS_NEXT)
-            pv(t, std::true_type{}, sc);
+            pv(st, std::true_type{}, sc);
         else
-            pv(t, std::false_type{}, sc);
+            pv(st, std::false_type{}, sc);
+        st = st1;
     };
 
     using T_ = std::true_type;
