@@ -68,6 +68,9 @@ constexpr int kBlockN = 64;                 // keys per tile
 constexpr int kStages = 3;                  // LDS ring depth
 constexpr int kAhead = kStages - 1;         // tiles in flight
 constexpr float kRescaleThreshold = 8.0f;   // log2 units
+// Largest sum of one lane's 16 weights of a key half accepted against a
+// speculative reference (the same bound on each weight as kRescaleThreshold).
+constexpr float kSpecLimit = 256.f;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -361,15 +364,15 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     bf16x8 p[4];
     float alpha = 1.f;
     bool upd = false;
-    // softmax state carried from phase X into phase Y of a step
-    float nm = 0.f, acc0 = 0.f, acc1 = 0.f;
+    // softmax state carried from phase X into phase Y of a step: -mref, the
+    // first half's weight sum, and the second half's partial sums
+    float nm = 0.f, acc0 = 0.f, acc1 = 0.f, acc2 = 0.f;
 
     // O^T += V^T P^T for the key tile in stage `st`: each MFMA's V fragment is read PF
     // MFMAs ahead; the order is pinned so that the waits stay PF deep.  With
-    // `tail`, the MFMAs carry the second half of the softmax of this tile
-    // (weights of S values 16..31, i.e. P operands 2 and 3): one piece after
-    // each of the first NV/2 MFMAs, so that P operand 2 is complete NV/4
-    // MFMAs before its first use and operand 3 NV/4 + 1 before its.
+    // `tail`, the MFMAs carry the weights of the second key half of this tile
+    // (P operands 2 and 3): one piece after each of the first NV/2 MFMAs,
+    // then the overflow check of that half, before P operand 2 is first used.
     auto pv = [&](int st, auto tail, const f32x16 (&sc)[2]) {
         constexpr bool TAIL = decltype(tail)::value;
         constexpr int TN = 32 / NV;  // weights per piece
@@ -385,16 +388,46 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
             if constexpr (TAIL) {
                 if (i < NV / 2) {
 #pragma unroll
-                    for (int e = 16 + i * TN; e < 16 + (i + 1) * TN; e += 2) {
-                        const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[e >> 4][e & 15], c, nm));
-                        const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[e >> 4][(e & 15) + 1], c, nm));
-                        p[e >> 3][e & 7] = (__bf16)x0;
-                        p[e >> 3][(e & 7) + 1] = (__bf16)x1;
-                        acc0 += x0;
-                        acc1 += x1;
+                    for (int e = i * TN; e < (i + 1) * TN; e += 2) {
+                        const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[1][e], c, nm));
+                        const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[1][e + 1], c, nm));
+                        p[2 + (e >> 3)][e & 7] = (__bf16)x0;
+                        p[2 + (e >> 3)][(e & 7) + 1] = (__bf16)x1;
+                        acc1 += x0;
+                        acc2 += x1;
                     }
-                } else if (i == NV / 2) {
-                    lsum = fmaf(lsum, alpha, acc0 + acc1);
+                }
+                if (i == NV / 2 - 1) {
+                    // second key half against the same reference: raise it
+                    // (and rescale everything accumulated so far, including
+                    // this tile's first half) if its weights overflow the limit
+                    __builtin_amdgcn_sched_barrier(0);
+                    float a2 = acc1 + acc2;
+                    const bool up2 = __builtin_amdgcn_ballot_w64(!(a2 <= kSpecLimit) && a2 == a2) != 0;
+                    if (up2) {
+                        float m1 = -INFINITY;
+#pragma unroll
+                        for (int e = 0; e < 16; ++e) m1 = fmaxf(m1, sc[1][e]);
+                        const float mnew = fmaxf(mref, pair_max(m1) * c);
+                        const float al = __builtin_amdgcn_exp2f(mref - mnew);
+                        mref = mnew;
+#pragma unroll
+                        for (int db = 0; db < DB; ++db) oacc[db] *= al;
+                        lsum *= al;
+                        acc0 *= al;
+                        acc1 = acc2 = 0.f;
+#pragma unroll
+                        for (int e = 0; e < 16; e += 2) {
+                            const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[1][e], c, -mnew));
+                            const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[1][e + 1], c, -mnew));
+                            p[2 + (e >> 3)][e & 7] = (__bf16)x0;
+                            p[2 + (e >> 3)][(e & 7) + 1] = (__bf16)x1;
+                            acc1 += x0;
+                            acc2 += x1;
+                        }
+                        a2 = acc1 + acc2;
+                    }
+                    lsum += acc0 + a2;
                 }
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -403,21 +436,24 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 
 
     // Phase X of a tile that has a successor: S_{t+1} = K_{t+1} Q^T on the
-    // MFMA pipe, and the first half of the softmax of S_t cut into pieces
-    // placed one after each MFMA (max: NK/4 pieces, reference update: 1,
-    // weights of S values 0..15 = P operands 0 and 1: NK/2), with K fragments
-    // read PF MFMAs ahead.  The other half runs beside the P V products.
+    // MFMA pipe, and beside it the weights of the first key half of S_t
+    // (P operands 0 and 1), one pair after every NK/8-th MFMA, with K
+    // fragments read PF MFMAs ahead.  The weights are taken against the
+    // current reference without a tile max: if some lane's 16 weights sum to
+    // more than kSpecLimit (a jump of the running max, or the first tile,
+    // where mref = -inf), the exact max of the tile is taken, the reference
+    // raised and the weights recomputed, outside the MFMA stream.  Weights
+    // then stay <= kSpecLimit, as with a lazily raised exact max.
     auto qk_softmax = [&](int st_next, const f32x16 (&sc)[2], f32x16 (&sn)[2]) {
         const lds_char *kt = stage_ptr(st_next);
         // The two waves sharing a SIMD contend for its MFMA pipe; the one in
         // this (VALU-heavy) phase goes first, and the other's P V products
         // fill the gaps between its MFMAs.
         __builtin_amdgcn_s_setprio(1);
-        constexpr int MAXP = NK / 4, EXPP = NK / 2;
-        constexpr int MAXN = 32 / MAXP, EXPN = 16 / EXPP;  // values per piece
+        constexpr int STRIDE = NK / 8;
         bf16x8 kr[PF];
-        float m0 = -INFINITY, m1 = -INFINITY;
         acc0 = acc1 = 0.f;
+        const float nm0 = -mref;
 #pragma unroll
         for (int i = 0; i < PF; ++i) kr[i] = kfrag(kt, i);
         __builtin_amdgcn_sched_barrier(0);
@@ -428,36 +464,48 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
             else
                 sn[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kr[i % PF], qf[i >> 1], sn[i & 1], 0, 0, 0);
             if (i + PF < NK) kr[i % PF] = kfrag(kt, i + PF);
-            if (i < MAXP) {
-#pragma unroll
-                for (int e = i * MAXN; e < (i + 1) * MAXN; e += 2) {
-                    m0 = fmaxf(m0, sc[e >> 4][e & 15]);
-                    m1 = fmaxf(m1, sc[e >> 4][(e & 15) + 1]);
-                }
-            } else if (i == MAXP) {
-                const float mt = pair_max(fmaxf(m0, m1)) * c;
-                upd = __builtin_amdgcn_ballot_w64(mt > mref + kRescaleThreshold) != 0;
-                const float mnew = upd ? fmaxf(mref, mt) : mref;
-                alpha = __builtin_amdgcn_exp2f(mref - mnew);
-                mref = mnew;
-                nm = -mnew;
-            } else if (i < MAXP + 1 + EXPP) {
-                const int e0 = (i - MAXP - 1) * EXPN;
-#pragma unroll
-                for (int e = e0; e < e0 + EXPN; e += 2) {
-                    const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[e >> 4][e & 15], c, nm));
-                    const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[e >> 4][(e & 15) + 1], c, nm));
-                    p[e >> 3][e & 7] = (__bf16)x0;
-                    p[e >> 3][(e & 7) + 1] = (__bf16)x1;
-                    acc0 += x0;
-                    acc1 += x1;
-                }
+            if (i % STRIDE == STRIDE - 1) {
+                const int e = 2 * (i / STRIDE);
+                const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[0][e], c, nm0));
+                const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[0][e + 1], c, nm0));
+                p[e >> 3][e & 7] = (__bf16)x0;
+                p[e >> 3][(e & 7) + 1] = (__bf16)x1;
+                acc0 += x0;
+                acc1 += x1;
             }
             __builtin_amdgcn_sched_barrier(0);
         }
+        float a1 = acc0 + acc1;
         // keep this half of the softmax in this phase: without a use here the
-        // compiler sinks it past the rescale branch, next to the P V products
-        __asm__ volatile("" : : "v"(p[0]), "v"(p[1]), "v"(acc0), "v"(acc1), "v"(nm), "v"(alpha));
+        // compiler sinks it past the branch below, next to the P V products
+        __asm__ volatile("" : : "v"(p[0]), "v"(p[1]), "v"(a1));
+        upd = __builtin_amdgcn_ballot_w64(!(a1 <= kSpecLimit) && a1 == a1) != 0;
+        if (upd) {
+            float m0 = -INFINITY, m1 = -INFINITY;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                m0 = fmaxf(m0, sc[0][e]);
+                m1 = fmaxf(m1, sc[1][e]);
+            }
+            const float mnew = fmaxf(mref, pair_max(fmaxf(m0, m1)) * c);
+            alpha = __builtin_amdgcn_exp2f(mref - mnew);
+            mref = mnew;
+            lsum *= alpha;
+            acc0 = acc1 = 0.f;
+#pragma unroll
+            for (int e = 0; e < 16; e += 2) {
+                const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[0][e], c, -mnew));
+                const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[0][e + 1], c, -mnew));
+                p[e >> 3][e & 7] = (__bf16)x0;
+                p[e >> 3][(e & 7) + 1] = (__bf16)x1;
+                acc0 += x0;
+                acc1 += x1;
+            }
+            a1 = acc0 + acc1;
+        }
+        acc0 = a1;
+        acc1 = acc2 = 0.f;
+        nm = -mref;
     };
 
     // Prologue: kAhead tiles in flight; S of the first tile.
