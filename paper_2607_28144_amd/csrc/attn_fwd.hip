@@ -136,6 +136,24 @@ __device__ __forceinline__ float pair_sum(float x)
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Stores the bf16 pair (x0, x1) as weights j, j+1 of a P operand and adds
+// the two rounded values (as the P V product sees them) to r.  O is divided
+// by the sum of these rounded weights, so that it is a convex combination of
+// V rows with exactly the weights the MFMA used: a dominant key then returns
+// its V row without the up-to-2^-9 error of its own weight's rounding.  (A
+// dot2 against (1, 1) is one instruction per pair; unpacking the pair costs
+// four.)
+__device__ __forceinline__ void put_pair(bf16x8 &dst, int j, float x0, float x1, float &r)
+{
+    bf16x2 pk;
+    pk[0] = (__bf16)x0;
+    pk[1] = (__bf16)x1;
+    dst[j] = pk[0];
+    dst[j + 1] = pk[1];
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    r = __builtin_amdgcn_fdot2_f32_bf16(pk, ones, r, false);
+}
+
 // Online-softmax step for one 32-query block over one 64-key tile.
 //   s      : S^T accumulators of the two 32-key halves (raw q.k dot products);
 //            register i of half kb holds key kb*32 + (i/4)*8 + hi*4 + i%4 of
@@ -143,14 +161,15 @@ __device__ __forceinline__ float pair_sum(float x)
 //   c      : scale * log2(e)
 //   mref   : exponent reference (log2 units), raised lazily
 //   lsum   : running fp32 sum of exp2(s*c - mref) over this lane's keys (the
-//            unrounded weights: summing the bf16-rounded ones would move LSE
-//            by up to 2^-9 when few keys dominate)
+//            unrounded weights, for LSE: summing the bf16-rounded ones would
+//            move LSE by up to 2^-9 when few keys dominate)
+//   lrnd   : the same sum of the bf16-rounded weights (normalizes O)
 //   p      : bf16 P^T operands of the four 16-key MFMA steps of the tile
 //   alpha  : factor the O accumulator must be multiplied by (1 if unchanged)
 //   upd    : wave-uniform flag: some lane raised its reference
 // MASK: keys at or past Skv (only in the last tile) get weight exactly 0.
 template <bool MASK>
-__device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, float &mref, float &lsum,
+__device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, float &mref, float &lsum, float &lrnd,
                                               bf16x8 (&p)[4], float &alpha, bool &upd, int key0, int Skv)
 {
     const int hi = (threadIdx.x >> 5) & 1;
@@ -167,7 +186,7 @@ __device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, flo
     alpha = __builtin_amdgcn_exp2f(mref - mnew);
     mref = mnew;
     const float nm = -mnew;
-    float acc0 = 0.f, acc1 = 0.f;
+    float acc0 = 0.f, acc1 = 0.f, accr = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -178,12 +197,12 @@ __device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, flo
                 e0 = valid(kb, i) ? e0 : 0.f;
                 e1 = valid(kb, i + 1) ? e1 : 0.f;
             }
-            p[kb * 2 + (i >> 3)][i & 7] = (__bf16)e0;
-            p[kb * 2 + (i >> 3)][(i & 7) + 1] = (__bf16)e1;
+            put_pair(p[kb * 2 + (i >> 3)], i & 7, e0, e1, accr);
             acc0 += e0;
             acc1 += e1;
         }
     lsum = fmaf(lsum, alpha, acc0 + acc1);
+    lrnd = fmaf(lrnd, alpha, accr);
 }
 
 template <int N>
@@ -359,14 +378,15 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 
     const float c = a.scale * kLog2e;
     float mref = -INFINITY;
-    float lsum = 0.f;
+    float lsum = 0.f, lrnd = 0.f;
     f32x16 scur[2], snext[2];
     bf16x8 p[4];
     float alpha = 1.f;
     bool upd = false;
     // softmax state carried from phase X into phase Y of a step: -mref, the
-    // first half's weight sum, and the second half's partial sums
-    float nm = 0.f, acc0 = 0.f, acc1 = 0.f, acc2 = 0.f;
+    // first half's weight sum, the second half's partial sums, and the sums
+    // of the rounded weights of both halves
+    float nm = 0.f, acc0 = 0.f, acc1 = 0.f, acc2 = 0.f, rh1 = 0.f, rh2 = 0.f;
 
     // O^T += V^T P^T for the key tile in stage `st`: each MFMA's V fragment is read PF
     // MFMAs ahead; the order is pinned so that the waits stay PF deep.  With
@@ -391,8 +411,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
                     for (int e = i * TN; e < (i + 1) * TN; e += 2) {
                         const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[1][e], c, nm));
                         const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[1][e + 1], c, nm));
-                        p[2 + (e >> 3)][e & 7] = (__bf16)x0;
-                        p[2 + (e >> 3)][(e & 7) + 1] = (__bf16)x1;
+                        put_pair(p[2 + (e >> 3)], e & 7, x0, x1, rh2);
                         acc1 += x0;
                         acc2 += x1;
                     }
@@ -414,20 +433,22 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 #pragma unroll
                         for (int db = 0; db < DB; ++db) oacc[db] *= al;
                         lsum *= al;
+                        lrnd *= al;
                         acc0 *= al;
-                        acc1 = acc2 = 0.f;
+                        rh1 *= al;
+                        acc1 = acc2 = rh2 = 0.f;
 #pragma unroll
                         for (int e = 0; e < 16; e += 2) {
                             const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[1][e], c, -mnew));
                             const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[1][e + 1], c, -mnew));
-                            p[2 + (e >> 3)][e & 7] = (__bf16)x0;
-                            p[2 + (e >> 3)][(e & 7) + 1] = (__bf16)x1;
+                            put_pair(p[2 + (e >> 3)], e & 7, x0, x1, rh2);
                             acc1 += x0;
                             acc2 += x1;
                         }
                         a2 = acc1 + acc2;
                     }
                     lsum += acc0 + a2;
+                    lrnd += rh1 + rh2;
                 }
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -452,7 +473,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         __builtin_amdgcn_s_setprio(1);
         constexpr int STRIDE = NK / 8;
         bf16x8 kr[PF];
-        acc0 = acc1 = 0.f;
+        acc0 = acc1 = rh1 = 0.f;
         const float nm0 = -mref;
 #pragma unroll
         for (int i = 0; i < PF; ++i) kr[i] = kfrag(kt, i);
@@ -468,8 +489,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
                 const int e = 2 * (i / STRIDE);
                 const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[0][e], c, nm0));
                 const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[0][e + 1], c, nm0));
-                p[e >> 3][e & 7] = (__bf16)x0;
-                p[e >> 3][(e & 7) + 1] = (__bf16)x1;
+                put_pair(p[e >> 3], e & 7, x0, x1, rh1);
                 acc0 += x0;
                 acc1 += x1;
             }
@@ -478,7 +498,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         float a1 = acc0 + acc1;
         // keep this half of the softmax in this phase: without a use here the
         // compiler sinks it past the branch below, next to the P V products
-        __asm__ volatile("" : : "v"(p[0]), "v"(p[1]), "v"(a1));
+        __asm__ volatile("" : : "v"(p[0]), "v"(p[1]), "v"(a1), "v"(rh1));
         upd = __builtin_amdgcn_ballot_w64(!(a1 <= kSpecLimit) && a1 == a1) != 0;
         if (upd) {
             float m0 = -INFINITY, m1 = -INFINITY;
@@ -491,20 +511,20 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
             alpha = __builtin_amdgcn_exp2f(mref - mnew);
             mref = mnew;
             lsum *= alpha;
-            acc0 = acc1 = 0.f;
+            lrnd *= alpha;
+            acc0 = acc1 = rh1 = 0.f;
 #pragma unroll
             for (int e = 0; e < 16; e += 2) {
                 const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[0][e], c, -mnew));
                 const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[0][e + 1], c, -mnew));
-                p[e >> 3][e & 7] = (__bf16)x0;
-                p[e >> 3][(e & 7) + 1] = (__bf16)x1;
+                put_pair(p[e >> 3], e & 7, x0, x1, rh1);
                 acc0 += x0;
                 acc1 += x1;
             }
             a1 = acc0 + acc1;
         }
         acc0 = a1;
-        acc1 = acc2 = 0.f;
+        acc1 = acc2 = rh2 = 0.f;
         nm = -mref;
     };
 
@@ -538,7 +558,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
             issue_next(next_stage(st1));             // tile t+kAhead, into the stage tile t-1 used
             qk_softmax(st1, sc, sn);
         } else {
-            softmax_block<MASK>(sc, c, mref, lsum, p, alpha, upd, t * kBlockN, Skv);
+            softmax_block<MASK>(sc, c, mref, lsum, lrnd, p, alpha, upd, t * kBlockN, Skv);
         }
         // ---- O rescale (rare), outside the MFMA streams
         if (upd) {
@@ -575,10 +595,11 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         step(t, scur, snext, F_{}, F_{});
     wait_vmcnt<0>();  // the clamped trailing copies must land before the workgroup exits
 
-    // Epilogue: O = O^T / l, LSE = ln2 * (m_ref + log2 l); a split tile's
-    // unit writes its normalized partial to the workspace instead.
+    // Epilogue: O = O^T / l (l of the rounded weights), LSE = ln2 * (m_ref +
+    // log2 l) (l of the exact ones); a split tile's unit writes its
+    // normalized partial to the workspace instead.
     const float lt = pair_sum(lsum);
-    const float inv = 1.0f / lt;
+    const float inv = 1.0f / pair_sum(lrnd);
     const float lse_val = (mref + __log2f(lt)) * kLn2;
     if (qi < Sq) {
         if (slot >= 0) {

@@ -143,8 +143,57 @@ def test_ragged_shapes(Sq, Skv, D, out):
 
 def test_peaky_scores_exercise_the_running_max():
     """scale 8/sqrt(d): score spread ~8x larger, so the running max moves by
-    more than the lazy-rescale threshold many times along the key loop."""
+    more than the lazy-rescale threshold many times along the keys.  This
+    small launch is split into one-tile key ranges (the exact-max path of a
+    last tile, and the LSE fixup); the key-loop case follows."""
     run_and_check("peaky scale x8", 1, 3, 700, 1500, 128, 21, torch.float32, scale=8 / math.sqrt(128))
+
+
+def whole_tile_rows(H: int) -> int:
+    """Query count that gives exactly one 256-query tile per CU: such a launch
+    runs every tile whole (no key-range split), so every workgroup goes
+    through the steady-state key loop rather than one-tile units."""
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    assert n_cu % H == 0
+    return n_cu // H * 256
+
+
+def test_peaky_scores_in_the_key_loop():
+    """Peaky scores (scale 8/sqrt(d)) with one whole query tile per CU, so the
+    running max moves many times inside the steady-state key loop of every
+    workgroup (sampled rows)."""
+    H = 4
+    Sq = whole_tile_rows(H)
+    run_and_check("peaky scale x8, key loop", 1, H, Sq, 1500, 128, 22, torch.float32, scale=8 / math.sqrt(128),
+                  rows=sample_rows(Sq, 200, 22))
+
+
+@pytest.mark.parametrize("D", [128, 64])
+def test_score_jumps_in_either_key_half(D):
+    """Keys built to jump the running max by more than 8 (log2 units; median
+    ~14) at chosen places: the second 32-key half of tile 2 (rescale in the
+    middle of the P V products), the first half of tile 4 (rescale before
+    them) and the ragged last tile (exact-max path).  Queries share a
+    direction u; the jump keys are multiples of u, so (nearly) every query row
+    sees each jump.  One whole query tile per CU keeps every workgroup in the
+    steady-state key loop (sampled rows)."""
+    B, H, Skv = 1, 2, 6 * 64 + 20
+    Sq = whole_tile_rows(H)
+    rng = np.random.default_rng(31)
+    u = rng.standard_normal((1, 1, H, D))
+    qf = rng.standard_normal((B, Sq, H, D)) + u
+    kf = rng.standard_normal((B, Skv, H, D))
+    g = math.sqrt(128 / D)
+    for key, mult in ((2 * 64 + 40, 1.5), (4 * 64 + 8, 2.5), (6 * 64 + 11, 3.5)):
+        kf[:, key] = g * mult * u[0, 0] + 0.1 * rng.standard_normal((B, H, D))
+    vf = rng.standard_normal((B, Skv, H, D))
+    q, k, v = (synth.f32_to_bf16_bits(x.astype(np.float32)) for x in (qf, kf, vf))
+    scale = synth.default_scale(D)
+    o, lse = api().attn_fwd(dev(q), dev(k), dev(v), scale=scale, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    rows = sample_rows(Sq, 200, 31)
+    o_ref, lse_ref = oracle.attn(np.ascontiguousarray(q[:, rows]), k, v, scale)
+    assert_close(f"score jumps d={D}", host(o)[:, rows], o_ref, lse.cpu().numpy()[:, :, rows], lse_ref)
 
 
 def test_zero_scale_gives_value_mean():
