@@ -23,6 +23,16 @@
  * Conventions common to every entry point
  *   - Every data pointer is DEVICE memory owned by the caller; the library
  *     never frees, keeps or synchronizes on it.
+ *   - Scratch memory: when the query tiles of an attention call do not fill
+ *     whole rounds of the GPU's compute units, the leftover tiles are split
+ *     along the keys and their partial results combined by a second kernel.
+ *     Those partials live in a workspace of (split units) x 256 x (D + 1)
+ *     floats (16.9 MB for 12 heads x 10920 tokens at D = 128) that the call
+ *     takes, stream-ordered, from a per-device memory pool and returns to it,
+ *     stream-ordered, before it returns; the pool keeps that memory for
+ *     later calls until the process ends.  A failed pool allocation returns
+ *     REGENVC_ERR_HIP with nothing enqueued.  regenvc_lse_merge allocates
+ *     nothing.
  *   - Q/K/V/O are logical [B, S, H, D] with element strides for b, s and h
  *     (regenvc_tensor); the D axis is contiguous.  Token-major [B,S,H,D]
  *     and head-major [B,H,S,D] are both expressible.  Inputs are bf16.
