@@ -641,10 +641,14 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 
 // Log-sum-exp combination of the key-range partials of each split tile
 // (the same identity as the chunk merge): one thread per 4 dims of one row.
+// The partials are visited in batches of FB whose LSE and O loads are all
+// issued before any of them is used, combined online (running max, sum and
+// weighted O), so the loop is not a chain of dependent memory accesses.
 template <bool OUT_F32>
 __global__ __launch_bounds__(256) void split_fixup_kernel(AttnArgs a, AttnPlan pl)
 {
     constexpr int BM = kWaves * 32;
+    constexpr int FB = 8;
     const int per_row = a.D / 4;
     const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t rows = (int64_t)(pl.n_tiles - pl.n_dp) * BM;
@@ -659,16 +663,35 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(AttnArgs a, AttnPlan p
     const int qi = qt * BM + r;
     if (qi >= a.Sq) return;
     const int64_t u0 = (int64_t)j * pl.seg;
-    float m = -INFINITY;
-    for (int c = 0; c < pl.seg; ++c) m = fmaxf(m, pl.ws_lse[(u0 + c) * BM + r]);
-    float s = 0.f;
-    for (int c = 0; c < pl.seg; ++c) s += expf(pl.ws_lse[(u0 + c) * BM + r] - m);
-    const float L = m + logf(s);
+    float m = -INFINITY, s = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int c = 0; c < pl.seg; ++c) {
-        const float w = expf(pl.ws_lse[(u0 + c) * BM + r] - L);
-        acc += w * *reinterpret_cast<const f32x4 *>(pl.ws_o + ((u0 + c) * BM + r) * a.D + d);
+    for (int c0 = 0; c0 < pl.seg; c0 += FB) {
+        float l[FB];
+        f32x4 o[FB];
+#pragma unroll
+        for (int k = 0; k < FB; ++k) {
+            const int64_t u = u0 + min(c0 + k, pl.seg - 1);
+            l[k] = c0 + k < pl.seg ? pl.ws_lse[u * BM + r] : -INFINITY;
+            o[k] = *reinterpret_cast<const f32x4 *>(pl.ws_o + (u * BM + r) * a.D + d);
+        }
+        float mb = m;
+#pragma unroll
+        for (int k = 0; k < FB; ++k) mb = fmaxf(mb, l[k]);
+        // every key range holds at least one key, so mb is finite from the
+        // first batch on
+        const float sc = expf(m - mb);
+        s *= sc;
+        acc *= sc;
+#pragma unroll
+        for (int k = 0; k < FB; ++k) {
+            const float w = expf(l[k] - mb);
+            s += w;
+            acc += w * o[k];
+        }
+        m = mb;
     }
+    const float L = m + logf(s);
+    acc *= 1.0f / s;
     char *orow = static_cast<char *>(a.o) +
                  ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
     if constexpr (OUT_F32) {

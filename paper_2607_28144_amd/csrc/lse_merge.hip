@@ -17,9 +17,14 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // Log-sum-exp merge of chunk partials: one thread per 4 dims of one row.
+// Parts are visited in batches of MB whose LSE and O loads are all issued
+// before any is used, and combined online (running max, sum and weighted O).
+// A part with LSE = -inf (an empty chunk) has weight 0; if every part is
+// empty the row is O = 0, LSE = -inf.
 template <bool OUT_F32>
 __global__ __launch_bounds__(256) void lse_merge_kernel(MergeArgs a)
 {
+    constexpr int MB = 4;
     const int per_row = a.D / 4;
     const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t rows = (int64_t)a.B * a.Sq * a.H;
@@ -32,19 +37,36 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(MergeArgs a)
     const int b = (int)(bi / a.Sq);
     const int64_t li = ((int64_t)b * a.H + h) * a.Sq + i;
 
-    float m = -INFINITY;
-    for (int c = 0; c < a.num_parts; ++c) m = fmaxf(m, a.lse_parts[c][li]);
+    float m = -INFINITY, s = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int c0 = 0; c0 < a.num_parts; c0 += MB) {
+        float l[MB];
+        f32x4 o[MB];
+#pragma unroll
+        for (int k = 0; k < MB; ++k) {
+            const int c = min(c0 + k, a.num_parts - 1);
+            l[k] = c0 + k < a.num_parts ? a.lse_parts[c][li] : -INFINITY;
+            o[k] = *reinterpret_cast<const f32x4 *>(a.o_parts[c] + row * a.D + d);
+        }
+        float mb = m;
+#pragma unroll
+        for (int k = 0; k < MB; ++k) mb = fmaxf(mb, l[k]);
+        if (mb == -INFINITY) continue;  // nothing but empty parts so far
+        const float sc = expf(m - mb);  // 0 while m is still -inf
+        s *= sc;
+        acc *= sc;
+#pragma unroll
+        for (int k = 0; k < MB; ++k) {
+            const float w = expf(l[k] - mb);
+            s += w;
+            acc += w * o[k];
+        }
+        m = mb;
+    }
     float L = -INFINITY;
     if (m != -INFINITY) {
-        float s = 0.f;
-        for (int c = 0; c < a.num_parts; ++c) s += expf(a.lse_parts[c][li] - m);
         L = m + logf(s);
-        for (int c = 0; c < a.num_parts; ++c) {
-            const float w = expf(a.lse_parts[c][li] - L);
-            const f32x4 oc = *reinterpret_cast<const f32x4 *>(a.o_parts[c] + row * a.D + d);
-            acc += w * oc;
-        }
+        acc *= 1.0f / s;
     }
     char *orow = static_cast<char *>(a.o) + ((int64_t)b * a.o_sb + (int64_t)i * a.o_ss + (int64_t)h * a.o_sh) *
                                                 (OUT_F32 ? 4 : 2);
