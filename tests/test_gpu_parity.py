@@ -227,6 +227,33 @@ def test_head_major_layout_matches_token_major_bitwise():
     assert torch.equal(a, b) and torch.equal(la, lb)
 
 
+def test_key_value_rows_beyond_32_bit_offsets():
+    """K/V token strides of 2^24 + 8 elements put the rows of one 64-key tile
+    more than 2^31 bytes apart, past the 32-bit lane offsets of the fast copy
+    path: every tile goes through the 64-bit address path.  The result must be
+    bitwise the one of contiguous K/V (same arithmetic), and match the oracle
+    (sampled rows; one whole query tile per CU, so the key loop runs)."""
+    H, D, Skv = 2, 128, 70
+    Sq = whole_tile_rows(H)
+    q, k, v = synth.qkv(28, 1, H, Sq, Skv, D)
+    S = (1 << 24) + 8
+    wide = []
+    for x in (k, v):
+        buf = torch.empty((Skv - 1) * S + H * D, dtype=torch.bfloat16, device="cuda")
+        view = buf.as_strided((1, Skv, H, D), (Skv * S, S, D, 1))
+        view.copy_(dev(x))
+        wide.append(view)
+    scale = synth.default_scale(D)
+    o_w, l_w = api().attn_fwd(dev(q), wide[0], wide[1], scale=scale, out_dtype=torch.float32)
+    o_c, l_c = api().attn_fwd(dev(q), dev(k), dev(v), scale=scale, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert torch.equal(o_w, o_c) and torch.equal(l_w, l_c)
+    rows = sample_rows(Sq, 100, 28)
+    o_ref, l_ref = oracle.attn(np.ascontiguousarray(q[:, rows]), k, v, scale)
+    assert_close("K/V rows 2^24 + 8 elements apart", host(o_w)[:, rows], o_ref, l_w.cpu().numpy()[:, :, rows], l_ref)
+    del wide
+
+
 def test_head_subset_equals_slice_of_full_run():
     """Ulysses hands a GPU a subset of heads: computing it alone must equal the
     slice of the all-heads result.  The two launches may be planned differently
