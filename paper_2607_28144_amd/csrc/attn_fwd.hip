@@ -227,25 +227,29 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     const int hi = lane >> 5;   // which half of the wave
     const int col = lane & 31;  // query column owned in the 32x32 accumulators
 
-    // Work item of this workgroup: a whole query tile (data-parallel part) or
-    // one key range of a split tile.  Whole tiles are renumbered XCD-aware:
-    // workgroup i runs on XCD i % 8, and each XCD gets a contiguous range of
-    // tiles so that one head's tiles share an L2.
+    // Work item of this workgroup: one key range of a split tile (the first
+    // n_units workgroups, so that these short items start with the first
+    // round instead of trailing the last one) or a whole query tile.  Whole
+    // tiles are renumbered XCD-aware: workgroup i runs on XCD i % 8, i.e.
+    // whole tile j on XCD (j + n_units) % 8, a fixed rotation of j % 8; each
+    // XCD gets a contiguous range of tiles so that one head's tiles share an
+    // L2.
     int tile, kt0, kt1, slot;
     const int item = blockIdx.x;
-    if (item < pl.n_dp) {
-        const int xcd = item & 7;
-        tile = xcd * (pl.n_dp >> 3) + min(xcd, pl.n_dp & 7) + (item >> 3);
-        kt0 = 0;
-        kt1 = pl.n_kt;
-        slot = -1;
-    } else {
-        const int u = item - pl.n_dp;
+    if (item < pl.n_units) {
+        const int u = item;
         const int sgi = u % pl.seg;
         tile = pl.n_dp + u / pl.seg;
         kt0 = (int)((int64_t)sgi * pl.n_kt / pl.seg);
         kt1 = (int)((int64_t)(sgi + 1) * pl.n_kt / pl.seg);
         slot = u;
+    } else {
+        const int j = item - pl.n_units;
+        const int xcd = j & 7;
+        tile = xcd * (pl.n_dp >> 3) + min(xcd, pl.n_dp & 7) + (j >> 3);
+        kt0 = 0;
+        kt1 = pl.n_kt;
+        slot = -1;
     }
     const int qt = tile % pl.n_qtiles;
     const int bh = tile / pl.n_qtiles;

@@ -28,7 +28,8 @@ struct AttnArgs {
 // each split into `seg` contiguous key ranges ("units", one workgroup each)
 // whose normalized partial O and LSE go to a workspace and are combined by a
 // log-sum-exp fixup.  Splitting only the leftover tiles keeps every CU busy
-// when the tile count is just above a multiple of the CU count.
+// when the tile count is just above a multiple of the CU count.  The units
+// are the first n_units workgroups of the grid, the whole tiles follow.
 struct AttnPlan {
     int32_t n_qtiles;  // query tiles per (batch, head)
     int32_t n_tiles;   // B * H * n_qtiles
