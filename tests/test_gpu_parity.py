@@ -283,6 +283,29 @@ def test_repeat_runs_are_bitwise_identical():
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
 
+def test_concurrent_calls_on_two_streams():
+    """Two split launches (each takes a workspace from the device pool) on
+    two streams at once, then the same two calls on one stream: results are
+    bitwise equal, so the calls neither share nor overwrite each other's
+    partials."""
+    q, k, v = synth.qkv(29, 1, 3, 700, 900, 128)
+    q2, k2, v2 = synth.qkv(30, 1, 3, 700, 900, 128)
+    inputs = [tuple(dev(x) for x in t) for t in ((q, k, v), (q2, k2, v2))]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = []
+    for s, (a, b, c) in zip(streams, inputs):
+        with torch.cuda.stream(s):
+            outs.append(api().attn_fwd(a, b, c, out_dtype=torch.float32))
+    torch.cuda.synchronize()
+    for (o, l), (a, b, c) in zip(outs, inputs):
+        o1, l1 = api().attn_fwd(a, b, c, out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        assert torch.equal(o, o1) and torch.equal(l, l1)
+    o_ref, l_ref = oracle.attn(q2, k2, v2, synth.default_scale(128))
+    assert_close("second stream", outs[1][0], o_ref, outs[1][1], l_ref)
+
+
 def test_empty_query_set_is_a_no_op():
     q, k, v = synth.qkv(27, 1, 2, 0, 64, 128)
     o, lse = api().attn_fwd(dev(q), dev(k), dev(v))
