@@ -7,7 +7,7 @@ a C ABI (include/regenvc_attn.h).  Import is cheap: the library and torch are
 loaded on first use.
 """
 
-__all__ = ["attn_fwd", "attn_partial_fwd", "lse_merge", "cross_attn_fwd", "RegenvcError"]
+__all__ = ["attn_fwd", "attn_partial_fwd", "lse_merge", "cross_attn_fwd", "attn_plan", "RegenvcError"]
 
 
 def __getattr__(name):

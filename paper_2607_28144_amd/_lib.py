@@ -17,6 +17,13 @@ class Tensor(ctypes.Structure):
                 ("stride_s", ctypes.c_int64), ("stride_h", ctypes.c_int64)]
 
 
+class AttnPlan(ctypes.Structure):
+    """regenvc_attn_plan: the work decomposition of one attention call."""
+    _fields_ = [("query_tiles", ctypes.c_int32), ("key_tiles", ctypes.c_int32),
+                ("whole_tiles", ctypes.c_int32), ("split_tiles", ctypes.c_int32),
+                ("key_ranges", ctypes.c_int32), ("workspace_bytes", ctypes.c_int64)]
+
+
 class RegenvcError(RuntimeError):
     def __init__(self, status: int, fn: str, detail: str):
         self.status = status
@@ -35,6 +42,7 @@ _SIGNATURES = {
                           _PT, ctypes.c_int, ctypes.c_void_p, _i32, _i32, _i32, _i32, ctypes.c_void_p],
     "regenvc_cross_attn_fwd": [_PT, _PT, _PT, _PT, ctypes.c_int, ctypes.c_void_p,
                                _i32, _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_void_p],
+    "regenvc_attn_plan_query": [_i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(AttnPlan)],
 }
 
 _lib = None

@@ -128,3 +128,13 @@ def lse_merge(o_parts: Sequence[torch.Tensor], lse_parts: Sequence[torch.Tensor]
         st = lib.regenvc_lse_merge(optrs, lptrs, n, ctypes.byref(od), _DT[out_dtype], lp, B, H, Sq, D, _stream(dev))
     _lib.check(st, "regenvc_lse_merge")
     return out, lse_out
+
+
+def attn_plan(B: int, H: int, Sq: int, Skv: int, D: int, n_cu: int = 256) -> dict:
+    """Work plan of one attention call of this shape on n_cu compute units
+    (regenvc_attn_plan_query; host-only): query/key tile counts, whole and
+    split query tiles, key ranges per split tile, workspace bytes."""
+    plan = _lib.AttnPlan()
+    st = _lib.load().regenvc_attn_plan_query(B, H, Sq, Skv, D, n_cu, ctypes.byref(plan))
+    _lib.check(st, "regenvc_attn_plan_query")
+    return {f: getattr(plan, f) for f, _ in _lib.AttnPlan._fields_}

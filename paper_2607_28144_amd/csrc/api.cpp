@@ -324,6 +324,27 @@ regenvc_status regenvc_lse_merge(const float *const *o_parts, const float *const
     return launched(regenvc::launch_merge(m, static_cast<hipStream_t>(stream)), "regenvc_lse_merge");
 }
 
+regenvc_status regenvc_attn_plan_query(int32_t B, int32_t H, int32_t Sq, int32_t Skv, int32_t D, int32_t n_cu,
+                                       regenvc_attn_plan *plan)
+{
+    if (plan == nullptr) return fail(REGENVC_ERR_INVALID_ARG, "regenvc_attn_plan_query: plan is NULL");
+    if (B < 0 || H < 0 || Sq < 0)
+        return fail(REGENVC_ERR_INVALID_ARG, "regenvc_attn_plan_query: negative size (B=%d H=%d Sq=%d)", B, H, Sq);
+    if (Skv < 1) return fail(REGENVC_ERR_INVALID_ARG, "regenvc_attn_plan_query: Skv=%d < 1", Skv);
+    if (n_cu < 1) return fail(REGENVC_ERR_INVALID_ARG, "regenvc_attn_plan_query: n_cu=%d < 1", n_cu);
+    if (D != 64 && D != 128) return fail(REGENVC_ERR_UNSUPPORTED, "regenvc_attn_plan_query: D=%d not in {64, 128}", D);
+    regenvc::AttnPlan pl{};
+    if (!regenvc::plan_attn(B, H, Sq, Skv, D, n_cu, &pl))
+        return fail(REGENVC_ERR_UNSUPPORTED, "regenvc_attn_plan_query: too many query tiles");
+    plan->query_tiles = pl.n_tiles;
+    plan->key_tiles = pl.n_kt;
+    plan->whole_tiles = pl.n_dp;
+    plan->split_tiles = pl.n_tiles - pl.n_dp;
+    plan->key_ranges = pl.n_units > 0 ? pl.seg : 0;
+    plan->workspace_bytes = (int64_t)regenvc::workspace_bytes(pl, D);
+    return REGENVC_OK;
+}
+
 const char *regenvc_status_str(regenvc_status status)
 {
     switch (status) {

@@ -783,14 +783,11 @@ template <int D, bool OUT_F32>
 hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream)
 {
     constexpr int BM = kWaves * 32;
-    const int64_t n_qtiles = (a.Sq + BM - 1) / BM;
-    const int64_t n_tiles = n_qtiles * a.H * a.B;
-    if (n_tiles > 0x7fffffff) return hipErrorInvalidConfiguration;
-    const int n_kt = (a.Skv + kBlockN - 1) / kBlockN;
-    AttnPlan pl = make_plan((int)n_qtiles, (int)n_tiles, n_kt, cu_count(), D);
+    AttnPlan pl{};
+    if (!plan_attn(a.B, a.H, a.Sq, a.Skv, D, cu_count(), &pl)) return hipErrorInvalidConfiguration;
     void *ws = nullptr;
     if (pl.n_units > 0) {
-        const size_t bytes = (size_t)pl.n_units * BM * (D + 1) * sizeof(float);
+        const size_t bytes = workspace_bytes(pl, D);
         hipMemPool_t pool = workspace_pool();
         hipError_t e = pool ? hipMallocFromPoolAsync(&ws, bytes, pool, stream) : hipErrorOutOfMemory;
         if (e != hipSuccess) return e;
@@ -814,6 +811,24 @@ hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream)
 }
 
 }  // namespace
+
+bool plan_attn(int B, int H, int Sq, int Skv, int D, int n_cu, AttnPlan *out)
+{
+    constexpr int BM = kWaves * 32;
+    if (B < 0 || H < 0 || Sq < 0 || Skv < 1 || n_cu < 1) return false;
+    const int64_t n_qtiles = ((int64_t)Sq + BM - 1) / BM;  // < 2^24
+    const int64_t per_batch = n_qtiles * H;                 // < 2^55: no overflow
+    if (per_batch > 0x7fffffff || (B > 0 && per_batch > 0x7fffffff / B)) return false;
+    const int64_t n_tiles = per_batch * B;
+    const int n_kt = (int)(((int64_t)Skv + kBlockN - 1) / kBlockN);
+    *out = make_plan((int)n_qtiles, (int)n_tiles, n_kt, n_cu, D);
+    return true;
+}
+
+size_t workspace_bytes(const AttnPlan &pl, int D)
+{
+    return (size_t)pl.n_units * (kWaves * 32) * (D + 1) * sizeof(float);
+}
 
 hipError_t launch_attn(const AttnArgs &a, hipStream_t stream)
 {

@@ -1,6 +1,7 @@
 // Internal launch interface between the C ABI layer and the gfx950 kernels.
 #pragma once
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 namespace regenvc {
@@ -58,6 +59,12 @@ struct FillArgs {  // empty-chunk partial: O = 0, LSE = -inf
     int64_t o_sb, o_ss, o_sh;
     int32_t B, H, Sq, D;
 };
+
+// Work plan of an attention launch of this shape on n_cu compute units
+// (host-only); false if the shape has no valid plan (Skv < 1, too many tiles).
+bool plan_attn(int B, int H, int Sq, int Skv, int D, int n_cu, AttnPlan *out);
+// Bytes of split-tile partials a plan needs (0 when nothing is split).
+size_t workspace_bytes(const AttnPlan &pl, int D);
 
 hipError_t launch_attn(const AttnArgs &a, hipStream_t stream);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t stream);

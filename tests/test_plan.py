@@ -1,0 +1,95 @@
+"""Host-only tests of the work plan (regenvc_attn_plan_query): the tile
+decomposition an attention call of a given shape uses, and the scratch
+memory it takes.  No GPU needed: the query makes no HIP call."""
+import ctypes
+
+import pytest
+
+from paper_2607_28144_amd import _lib
+from paper_2607_28144_amd.api import attn_plan
+
+BM, BN = 256, 64
+
+
+def ceil_div(a, b):
+    return -(-a // b)
+
+
+def check_invariants(p, B, H, Sq, Skv, D, n_cu):
+    assert p["query_tiles"] == B * H * ceil_div(Sq, BM)
+    assert p["key_tiles"] == ceil_div(Skv, BN)
+    assert p["whole_tiles"] + p["split_tiles"] == p["query_tiles"]
+    assert 0 <= p["split_tiles"] < n_cu
+    if p["split_tiles"]:
+        # only the tiles of a last, partial round over the compute units are split
+        assert p["whole_tiles"] % n_cu == 0
+        assert p["whole_tiles"] == (p["query_tiles"] // n_cu) * n_cu
+        assert 2 <= p["key_ranges"] <= p["key_tiles"]
+    else:
+        assert p["key_ranges"] == 0
+    units = p["split_tiles"] * p["key_ranges"]
+    assert p["workspace_bytes"] == units * BM * (D + 1) * 4
+
+
+def test_window_plan():
+    """12 heads x 10920 tokens (7 latent frames of 30 x 52): 516 query tiles on
+    256 CUs are two full rounds plus 4 tiles, which are split along the keys."""
+    p = attn_plan(1, 12, 10920, 10920, 128)
+    check_invariants(p, 1, 12, 10920, 10920, 128, 256)
+    assert p == {"query_tiles": 516, "key_tiles": 171, "whole_tiles": 512, "split_tiles": 4,
+                 "key_ranges": 29, "workspace_bytes": 15_323_136}
+
+
+def test_share_plan_splits_nothing():
+    """One sequence-parallel rank's share, 5 heads x 10920 queries against a
+    key chunk of 2730: 215 tiles fit in one round of 256 CUs."""
+    p = attn_plan(1, 5, 10920, 2730, 128)
+    check_invariants(p, 1, 5, 10920, 2730, 128, 256)
+    assert (p["key_tiles"], p["whole_tiles"], p["split_tiles"], p["workspace_bytes"]) == (43, 215, 0, 0)
+
+
+def test_cross_plan():
+    """Cross-attention to 512 context tokens: 8 key tiles, split one per range."""
+    p = attn_plan(1, 12, 10920, 512, 128)
+    check_invariants(p, 1, 12, 10920, 512, 128, 256)
+    assert (p["key_tiles"], p["split_tiles"], p["key_ranges"]) == (8, 4, 8)
+
+
+@pytest.mark.parametrize("B,H,Sq,Skv,D,n_cu", [
+    (1, 1, 1, 1, 64, 256), (1, 1, 256, 64, 128, 1), (2, 5, 1000, 3000, 64, 7),
+    (1, 12, 10920, 10920, 64, 256), (1, 12, 10920, 10920, 128, 304), (4, 24, 4096, 4096, 128, 256),
+    (1, 1, 300, 65536, 128, 256), (1, 12, 10920, 10920, 128, 80),
+])
+def test_plan_invariants(B, H, Sq, Skv, D, n_cu):
+    check_invariants(attn_plan(B, H, Sq, Skv, D, n_cu), B, H, Sq, Skv, D, n_cu)
+
+
+def test_single_key_tile_is_never_split():
+    p = attn_plan(1, 1, 300, 64, 128)
+    assert (p["whole_tiles"], p["split_tiles"], p["key_ranges"]) == (2, 0, 0)
+
+
+def test_empty_problem_plans_nothing():
+    for B, H, Sq in [(0, 12, 10920), (1, 0, 10920), (1, 12, 0)]:
+        p = attn_plan(B, H, Sq, 10920, 128)
+        assert p["query_tiles"] == 0 and p["whole_tiles"] == 0 and p["split_tiles"] == 0
+        assert p["workspace_bytes"] == 0
+
+
+@pytest.mark.parametrize("args,status", [
+    ((-1, 1, 1, 1, 128, 256), 1), ((1, -1, 1, 1, 128, 256), 1), ((1, 1, -1, 1, 128, 256), 1),
+    ((1, 1, 1, 0, 128, 256), 1), ((1, 1, 1, 1, 128, 0), 1),
+    ((1, 1, 1, 1, 96, 256), 2), ((1, 1, 1, 1, 256, 256), 2),
+    ((2**31 - 1, 2**31 - 1, 2**31 - 1, 1, 128, 256), 2),
+])
+def test_bad_arguments_leave_the_plan_untouched(args, status):
+    lib = _lib.load()
+    plan = _lib.AttnPlan(query_tiles=-7, workspace_bytes=-7)
+    assert lib.regenvc_attn_plan_query(*args, ctypes.byref(plan)) == status
+    assert plan.query_tiles == -7 and plan.workspace_bytes == -7
+    assert lib.regenvc_last_error().decode().startswith("regenvc_attn_plan_query")
+
+
+def test_null_plan_is_rejected():
+    lib = _lib.load()
+    assert lib.regenvc_attn_plan_query(1, 1, 1, 1, 128, 256, None) == 1
