@@ -50,6 +50,12 @@
  *   - All entry points are reentrant; concurrent calls on different streams
  *     are independent.
  *   - The same launch configuration gives bit-identical results run to run.
+ *   - Two schedules of the attention kernel exist; a launch whose key range
+ *     spans at least 32 tiles of 64 keys uses the ping-pong one, a shorter
+ *     one the interleaved one.  They compute the same quantities with a
+ *     different summation order (results agree to rounding, not bitwise).
+ *     The environment variable REGENVC_ATTN_SCHEDULE=pingpong|interleaved,
+ *     read at each call, forces one of them (diagnostics and tests).
  */
 #ifndef REGENVC_ATTN_H
 #define REGENVC_ATTN_H

@@ -12,8 +12,8 @@
 //               the other's matrix instructions.
 //   wave      = 32 queries, all head dims, every key tile.
 //   key tile  = 64 keys.  K and V tiles are copied HBM -> LDS with
-//               global_load_lds_dwordx4 (no register staging) into a 3-stage
-//               ring: two tiles in flight, one barrier per tile.
+//               global_load_lds_dwordx4 (no register staging) into a ring of
+//               LDS stages (3 in the interleaved schedule, 4 in ping-pong).
 //   Workgroups are renumbered so that the tiles of one head run on the same
 //   XCD (each XCD has its own L2; the hardware deals workgroups round-robin).
 //
@@ -27,12 +27,16 @@
 //   with ds_read_b64_tr_b16 in that key order.  Attention is invariant under
 //   a joint permutation of keys and values, so no shuffle is needed.
 //
-// Software pipeline (per wave, tile t):
-//   phase X:  MFMA  S_{t+1} = K_{t+1} Q^T
-//             VALU  softmax of S_t
-//   phase Y:  MFMA  O^T += V_t^T P_t^T
-//   the exponentials of tile t run beside the Q K^T products of tile t+1 (and
-//   beside the other wave's MFMAs on the same SIMD).
+// Two schedules of the key loop (the launch picks one by the number of key
+// tiles; results agree to rounding):
+//   interleaved (attn_fwd_kernel), per wave and tile t:
+//     phase X:  MFMA  S_{t+1} = K_{t+1} Q^T   beside  VALU  softmax of S_t
+//     phase Y:  MFMA  O^T += V_t^T P_t^T       beside  the rest of it
+//   ping-pong (attn_fwd_pingpong_kernel): each wave alternates a pure MFMA
+//     phase (P V of the previous tile, then Q K^T of the current one) and a
+//     pure VALU phase (the weights), the two waves of a SIMD in opposite
+//     phases, separated by workgroup barriers; faster on long key ranges,
+//     slower on short ones (longer prologue, two barriers per tile).
 //
 // Lazy rescaling: the running max used as the exponent reference is only
 //   raised when a tile's max exceeds it by more than 8 (log2 units); the
@@ -47,6 +51,8 @@
 
 #include <atomic>
 #include <cstdint>
+#include <cstdlib>
+#include <cstring>
 #include <mutex>
 #include <type_traits>
 
@@ -65,8 +71,15 @@ typedef __attribute__((address_space(3))) char lds_char;
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kBlockN = 64;                 // keys per tile
-constexpr int kStages = 3;                  // LDS ring depth
-constexpr int kAhead = kStages - 1;         // tiles in flight
+constexpr int kStages = 3;                  // LDS ring depth (interleaved schedule)
+constexpr int kAhead = kStages - 1;         // tiles in flight (interleaved schedule)
+constexpr int kStagesPP = 4;                // LDS ring depth (ping-pong schedule)
+// Launches whose work items span at least this many key tiles use the
+// ping-pong schedule; shorter ones (cross-attention to a few hundred
+// context tokens) the interleaved one, whose prologue and epilogue are
+// shorter (measured: ping-pong 2.5 % faster at 171 key tiles, 1 % at 43,
+// 6.6 % slower at 8).
+constexpr int kPingPongMinTiles = 32;
 constexpr float kRescaleThreshold = 8.0f;   // log2 units
 // Largest sum of one lane's 16 weights of a key half accepted against a
 // speculative reference (the same bound on each weight as kRescaleThreshold).
@@ -74,14 +87,14 @@ constexpr float kSpecLimit = 256.f;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-template <int D>
+template <int D, int STAGES = kStages>
 struct Geo {
     static constexpr int NCH = D / 8;                      // 16-byte chunks per row
     static constexpr int DS = D / 16;                      // k-steps of Q K^T
     static constexpr int DB = D / 32;                      // 32-row blocks of O^T
     static constexpr int TILE = kBlockN * D * 2;           // bytes of one K or V tile
     static constexpr int STAGE = 2 * TILE;                 // K tile then V tile
-    static constexpr int LDS = kStages * STAGE;
+    static constexpr int LDS = STAGES * STAGE;
     static constexpr int LOADS = kBlockN * NCH / kThreads; // 16-byte loads per thread per tensor per tile
     static_assert(LOADS >= 1 && (kBlockN * NCH) % kThreads == 0, "tile load split");
 };
@@ -122,6 +135,42 @@ __device__ __forceinline__ void lds_dma16_s(const void *gbase, uint32_t off, uin
                      :
                      : "s"(base), "v"(off), "s"((const void *)(uintptr_t)gs)
                      : "m0");
+}
+
+// The LOADS copies of one tile tensor by this thread with a wave-uniform
+// source base and LDS address: lane offsets off[j], LDS block j at
+// lds_base + j KB.  M0 is set once per group; the immediate offset (applied
+// to the global and the LDS address alike) steps the LDS block, and the
+// scalar base is lowered by the same amount so that the global address is
+// base + off[j].  The leading nop covers a scalar base written just before by
+// a vector instruction (readfirstlane).
+template <int LOADS>
+__device__ __forceinline__ void lds_dma16_group(const uint16_t *base, const uint32_t (&off)[LOADS], uint32_t lds_base)
+{
+    const char *b = reinterpret_cast<const char *>(base);
+    if constexpr (LOADS == 1) {
+        __asm__ volatile("s_nop 4\n\ts_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                         :
+                         : "s"(lds_base), "v"(off[0]), "s"(b)
+                         : "m0");
+    } else {
+        static_assert(LOADS == 2, "copy group of one or two chunks");
+        __asm__ volatile("s_nop 4\n\ts_mov_b32 m0, %0\n\t"
+                         "global_load_lds_dwordx4 %1, %3\n\t"
+                         "global_load_lds_dwordx4 %2, %4 offset:1024"
+                         :
+                         : "s"(lds_base), "v"(off[0]), "v"(off[1]), "s"(b), "s"(b - 1024)
+                         : "m0");
+    }
+}
+
+// A pointer the caller knows to be wave-uniform, moved to scalar registers.
+__device__ __forceinline__ const uint16_t *uniform_ptr(const uint16_t *p)
+{
+    const uint64_t g = (uint64_t)(uintptr_t)p;
+    const uint32_t ghi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(g >> 32));
+    const uint32_t glo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)g);
+    return (const uint16_t *)(uintptr_t)(((uint64_t)ghi << 32) | (uint64_t)glo);
 }
 
 // (x of this lane, x of lane^32) combined so both halves hold the same value.
@@ -205,6 +254,87 @@ __device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, flo
     lrnd = fmaf(lrnd, alpha, accr);
 }
 
+// Work item of a workgroup: one key range of a split tile (the first
+// n_units workgroups, so that these short items start with the first round
+// instead of trailing the last one) or a whole query tile.  Whole tiles are
+// renumbered XCD-aware: workgroup i runs on XCD i % 8, i.e. whole tile j on
+// XCD (j + n_units) % 8, a fixed rotation of j % 8; each XCD gets a
+// contiguous range of tiles so that one head's tiles share an L2.
+struct WorkItem {
+    int tile, kt0, kt1, slot;  // slot: workspace row block of a key range, -1 for a whole tile
+};
+__device__ __forceinline__ WorkItem work_item(const AttnPlan &pl, int item)
+{
+    WorkItem w;
+    if (item < pl.n_units) {
+        const int sgi = item % pl.seg;
+        w.tile = pl.n_dp + item / pl.seg;
+        w.kt0 = (int)((int64_t)sgi * pl.n_kt / pl.seg);
+        w.kt1 = (int)((int64_t)(sgi + 1) * pl.n_kt / pl.seg);
+        w.slot = item;
+    } else {
+        const int j = item - pl.n_units;
+        const int xcd = j & 7;
+        w.tile = xcd * (pl.n_dp >> 3) + min(xcd, pl.n_dp & 7) + (j >> 3);
+        w.kt0 = 0;
+        w.kt1 = pl.n_kt;
+        w.slot = -1;
+    }
+    return w;
+}
+
+// Epilogue of one lane's query row: O = O^T / l with l the sum of the
+// bf16-rounded weights (the ones the P V products used), LSE = ln2 * (m_ref +
+// log2 l') with l' the sum of the exact weights; a split tile's key range
+// writes its normalized partial to the workspace instead.  lsum, lrnd are
+// this lane's halves (the other half is in lane^32).
+template <int D, bool OUT_F32>
+__device__ __forceinline__ void store_row(const AttnArgs &a, const AttnPlan &pl, const f32x16 (&oacc)[D / 32],
+                                          float lsum, float lrnd, float mref, int b, int h, int qi, int qrow, int slot)
+{
+    constexpr int BM = kWaves * 32;
+    constexpr int DB = D / 32;
+    const int hi = (threadIdx.x >> 5) & 1;
+    const float lt = pair_sum(lsum);
+    const float inv = 1.0f / pair_sum(lrnd);
+    const float lse_val = (mref + __log2f(lt)) * kLn2;
+    if (qi >= a.Sq) return;
+    if (slot >= 0) {
+        float *orow = pl.ws_o + ((int64_t)slot * BM + qrow) * D;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int gq = 0; gq < 4; ++gq) {
+                f32x4 w;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) w[e] = oacc[db][gq * 4 + e] * inv;
+                *reinterpret_cast<f32x4 *>(orow + db * 32 + gq * 8 + hi * 4) = w;
+            }
+        if (hi == 0) pl.ws_lse[(int64_t)slot * BM + qrow] = lse_val;
+    } else {
+        char *orow = static_cast<char *>(a.o) +
+                     ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int gq = 0; gq < 4; ++gq) {
+                const int d = db * 32 + gq * 8 + hi * 4;
+                if constexpr (OUT_F32) {
+                    f32x4 w;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) w[e] = oacc[db][gq * 4 + e] * inv;
+                    *reinterpret_cast<f32x4 *>(orow + d * 4) = w;
+                } else {
+                    bf16x4 w;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) w[e] = (__bf16)(oacc[db][gq * 4 + e] * inv);
+                    *reinterpret_cast<bf16x4 *>(orow + d * 2) = w;
+                }
+            }
+        if (a.lse != nullptr && hi == 0) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = lse_val;
+    }
+}
+
 template <int N>
 __device__ __forceinline__ void wait_vmcnt()
 {
@@ -227,30 +357,8 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     const int hi = lane >> 5;   // which half of the wave
     const int col = lane & 31;  // query column owned in the 32x32 accumulators
 
-    // Work item of this workgroup: one key range of a split tile (the first
-    // n_units workgroups, so that these short items start with the first
-    // round instead of trailing the last one) or a whole query tile.  Whole
-    // tiles are renumbered XCD-aware: workgroup i runs on XCD i % 8, i.e.
-    // whole tile j on XCD (j + n_units) % 8, a fixed rotation of j % 8; each
-    // XCD gets a contiguous range of tiles so that one head's tiles share an
-    // L2.
-    int tile, kt0, kt1, slot;
-    const int item = blockIdx.x;
-    if (item < pl.n_units) {
-        const int u = item;
-        const int sgi = u % pl.seg;
-        tile = pl.n_dp + u / pl.seg;
-        kt0 = (int)((int64_t)sgi * pl.n_kt / pl.seg);
-        kt1 = (int)((int64_t)(sgi + 1) * pl.n_kt / pl.seg);
-        slot = u;
-    } else {
-        const int j = item - pl.n_units;
-        const int xcd = j & 7;
-        tile = xcd * (pl.n_dp >> 3) + min(xcd, pl.n_dp & 7) + (j >> 3);
-        kt0 = 0;
-        kt1 = pl.n_kt;
-        slot = -1;
-    }
+    const WorkItem wi = work_item(pl, blockIdx.x);
+    const int tile = wi.tile, kt0 = wi.kt0, kt1 = wi.kt1, slot = wi.slot;
     const int qt = tile % pl.n_qtiles;
     const int bh = tile / pl.n_qtiles;
     const int h = bh % a.H;
@@ -599,48 +707,340 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         step(t, scur, snext, F_{}, F_{});
     wait_vmcnt<0>();  // the clamped trailing copies must land before the workgroup exits
 
-    // Epilogue: O = O^T / l (l of the rounded weights), LSE = ln2 * (m_ref +
-    // log2 l) (l of the exact ones); a split tile's unit writes its
-    // normalized partial to the workspace instead.
-    const float lt = pair_sum(lsum);
-    const float inv = 1.0f / pair_sum(lrnd);
-    const float lse_val = (mref + __log2f(lt)) * kLn2;
-    if (qi < Sq) {
-        if (slot >= 0) {
-            float *orow = pl.ws_o + ((int64_t)slot * BM + qrow) * D;
+    store_row<D, OUT_F32>(a, pl, oacc, lsum, lrnd, mref, b, h, qi, qrow, slot);
+}
+
+// Ping-pong schedule of the same computation (launches with many key tiles).
+// Waves w and w+4 share a SIMD; group 0 (waves 0-3) and group 1 (waves 4-7)
+// alternate, in opposite phases, between
+//   M(u): a straight MFMA stream: O^T += V^T P^T of tile u-1, then
+//         S^T = K Q^T of tile u, operand fragments read PF MFMAs ahead;
+//   V(u): the weights of tile u (vector instructions only),
+// with a workgroup barrier between phases, so that on every SIMD one wave
+// streams MFMAs while the other computes weights.  (A wave that interleaves
+// its own weights with its MFMAs keeps the matrix pipe about half busy; two
+// waves in opposite phases keep it about 80 % busy in a probe of the same
+// instruction mix.)  Tiles go through a 4-stage LDS ring: each wave copies its
+// share of tile u+2 right after M(u), into the stage of tile u-2.
+//
+// Weights use the speculative reference of the interleaved kernel, checked
+// once per tile (a lane's 32 weights summing to more than kSpecLimit), and
+// the same two running sums; the sum of the bf16-rounded weights is formed by
+// unpacking the pairs (the dot2 instructions would occupy the matrix pipe the
+// other wave is streaming on).
+template <int D, bool OUT_F32>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
+{
+    using G = Geo<D, kStagesPP>;
+    constexpr int NCH = G::NCH, DS = G::DS, DB = G::DB, LOADS = G::LOADS;
+    constexpr int BM = kWaves * 32;
+    constexpr int PER_TILE = 2 * LOADS;  // copies per thread per tile (K and V)
+    static_assert(kStagesPP == 4, "tile u+2 is copied into the stage of tile u-2");
+
+    __shared__ __attribute__((aligned(1024))) char smem[G::LDS];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
+    const int grp = wave >> 2;
+    const int hi = lane >> 5;
+    const int col = lane & 31;
+
+    const WorkItem wi = work_item(pl, blockIdx.x);
+    const int tile = wi.tile, kt0 = wi.kt0, kt1 = wi.kt1, slot = wi.slot;
+    const int qt = tile % pl.n_qtiles;
+    const int bh = tile / pl.n_qtiles;
+    const int h = bh % a.H;
+    const int b = bh / a.H;
+    const int qrow = wave * 32 + col;
+    const int qi = qt * BM + qrow;
+
+    const uint16_t *qp = static_cast<const uint16_t *>(a.q) + b * a.q_sb + h * a.q_sh;
+    const uint16_t *kp = static_cast<const uint16_t *>(a.k) + b * a.k_sb + h * a.k_sh;
+    const uint16_t *vp = static_cast<const uint16_t *>(a.v) + b * a.v_sb + h * a.v_sh;
+    const int Skv = a.Skv;
+    const int T = kt1 - kt0;  // key tiles of this work item, >= 1
+    const bool ragged_end = kt1 == pl.n_kt && (Skv % kBlockN) != 0;
+
+    bf16x8 qf[DS];
 #pragma unroll
-            for (int db = 0; db < DB; ++db)
-#pragma unroll
-                for (int gq = 0; gq < 4; ++gq) {
-                    f32x4 w;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) w[e] = oacc[db][gq * 4 + e] * inv;
-                    *reinterpret_cast<f32x4 *>(orow + db * 32 + gq * 8 + hi * 4) = w;
-                }
-            if (hi == 0) pl.ws_lse[(int64_t)slot * BM + qrow] = lse_val;
-        } else {
-            char *orow = static_cast<char *>(a.o) +
-                         ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
-#pragma unroll
-            for (int db = 0; db < DB; ++db)
-#pragma unroll
-                for (int gq = 0; gq < 4; ++gq) {
-                    const int d = db * 32 + gq * 8 + hi * 4;
-                    if constexpr (OUT_F32) {
-                        f32x4 w;
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) w[e] = oacc[db][gq * 4 + e] * inv;
-                        *reinterpret_cast<f32x4 *>(orow + d * 4) = w;
-                    } else {
-                        bf16x4 w;
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) w[e] = (__bf16)(oacc[db][gq * 4 + e] * inv);
-                        *reinterpret_cast<bf16x4 *>(orow + d * 2) = w;
-                    }
-                }
-            if (a.lse != nullptr && hi == 0) a.lse[((int64_t)b * a.H + h) * Sq + qi] = lse_val;
-        }
+    for (int ds = 0; ds < DS; ++ds) {
+        if (qi < a.Sq)
+            qf[ds] = *reinterpret_cast<const bf16x8 *>(qp + (int64_t)qi * a.q_ss + ds * 16 + hi * 8);
+        else
+            qf[ds] = bf16x8{};
     }
+
+    // HBM -> LDS copies, as in the interleaved kernel: tiles in order kt0,
+    // kt0+1, ... (one call per tile, into ring stages 0, 1, 2, ...), the last
+    // one repeated into otherwise unused stages, so that every call issues
+    // exactly PER_TILE copies per thread and the vmcnt waits count tiles.
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char *)smem;
+    uint32_t kofs[LOADS], vofs[LOADS];
+#pragma unroll
+    for (int j = 0; j < LOADS; ++j) {
+        const int slot16 = (wave * LOADS + j) * 64 + lane;
+        const int row = slot16 / NCH, phys = slot16 % NCH;
+        kofs[j] = (uint32_t)((row * a.k_ss + k_slot<NCH>(row, phys) * 8) * 2);
+        vofs[j] = (uint32_t)((row * a.v_ss + v_slot<NCH>(row, phys) * 8) * 2);
+    }
+    const int64_t k_step = (int64_t)kBlockN * a.k_ss, v_step = (int64_t)kBlockN * a.v_ss;
+    const int last_full = Skv / kBlockN - 1;  // last tile with kBlockN keys
+    int tl_copy = kt0;
+    int st_copy = 0;
+    const uint16_t *kb_copy = kp + kt0 * k_step;
+    const uint16_t *vb_copy = vp + kt0 * v_step;
+    auto issue_next = [&]() __attribute__((always_inline)) {
+        const uint32_t kdst = lds0 + st_copy * G::STAGE;
+        const uint32_t vdst = kdst + G::TILE;
+        if (a.kv_off32 && tl_copy <= last_full) {
+            const uint32_t blk = __builtin_amdgcn_readfirstlane(wave * LOADS * 1024);
+            lds_dma16_group<LOADS>(uniform_ptr(kb_copy), kofs, __builtin_amdgcn_readfirstlane(kdst) + blk);
+            lds_dma16_group<LOADS>(uniform_ptr(vb_copy), vofs, __builtin_amdgcn_readfirstlane(vdst) + blk);
+        } else {
+            const int key0 = tl_copy * kBlockN;
+            const int last = Skv - 1 - key0;
+#pragma unroll
+            for (int j = 0; j < LOADS; ++j) {
+                const int blk = wave * LOADS + j;
+                const int slot16 = blk * 64 + lane;
+                const int row = slot16 / NCH, phys = slot16 % NCH;
+                const int64_t key = key0 + min(row, last);
+                lds_dma16(kp + key * a.k_ss + k_slot<NCH>(row, phys) * 8, kdst + blk * 1024);
+                lds_dma16(vp + key * a.v_ss + v_slot<NCH>(row, phys) * 8, vdst + blk * 1024);
+            }
+        }
+        st_copy = st_copy == kStagesPP - 1 ? 0 : st_copy + 1;
+        if (tl_copy < kt1 - 1) {
+            ++tl_copy;
+            kb_copy += k_step;
+            vb_copy += v_step;
+        }
+    };
+
+    // Per-lane LDS byte offsets of the MFMA operand fragments (stage 0), as
+    // in the interleaved kernel.
+    int koff[DS];
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) koff[ds] = (col * D + k_slot<NCH>(col, ds * 2 + hi) * 8) * 2;
+    const int g = lane >> 4, x = lane & 15;
+    int voff[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+        const int row = 4 * (g >> 1) + (x >> 2);
+        const int dcol = db * 32 + 16 * (g & 1) + 4 * (x & 3);
+        voff[db] = G::TILE + (row * D + v_slot<NCH>(row, dcol >> 3) * 8 + (dcol & 7)) * 2;
+    }
+    constexpr int NK = 2 * DS;  // K fragments (MFMAs) per tile for S^T
+    constexpr int NV = 4 * DB;  // V fragments (MFMAs) per tile for O^T
+    constexpr int PF = 4;       // fragments read ahead of their MFMA
+    static_assert(NK >= PF && NV >= PF, "schedule assumes d >= 64");
+    auto kfrag = [&](const lds_char *kt, int i) -> bf16x8 {
+        return *(const lds_bf16x8 *)(kt + koff[i >> 1] + (i & 1) * 32 * D * 2);
+    };
+    auto vfrag = [&](const lds_char *vt, int i) -> bf16x8 {
+        const int kk = i / DB, db = i % DB;
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(vt + voff[db] + kk * 16 * D * 2));
+        const bf16x4 up =
+            __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(vt + voff[db] + (kk * 16 + 8) * D * 2));
+        return bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
+    };
+    auto stage_ptr = [&](int st) { return (const lds_char *)(smem + st * G::STAGE); };
+
+    f32x16 oacc[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) oacc[db] = f32x16{};
+    f32x16 s[2];
+    bf16x8 p[4];
+    const float c = a.scale * kLog2e;
+    float mref = -INFINITY, lsum = 0.f, lrnd = 0.f;
+
+    // M phase: PV of the tile in stage stv (weights p), then QK of the tile in
+    // stage stq (into s); the order is pinned so the fragment reads stay PF
+    // MFMAs ahead.
+    auto mphase = [&](int stq, int stv, auto do_pv, auto do_qk) __attribute__((always_inline)) {
+        constexpr bool PV = decltype(do_pv)::value, QK = decltype(do_qk)::value;
+        constexpr int N0 = PV ? NV : 0;
+        constexpr int N = N0 + (QK ? NK : 0);
+        const lds_char *vt = stage_ptr(stv);
+        const lds_char *kt = stage_ptr(stq);
+        auto frag = [&](int j) -> bf16x8 { return j < N0 ? vfrag(vt, j) : kfrag(kt, j - N0); };
+        bf16x8 r[PF];
+#pragma unroll
+        for (int j = 0; j < PF; ++j) r[j] = frag(j);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < N; ++j) {
+            if (j < N0) {
+                oacc[j % DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(r[j % PF], p[j / DB], oacc[j % DB], 0, 0, 0);
+            } else {
+                const int i = j - N0;
+                s[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(r[j % PF], qf[i >> 1], i < 2 ? f32x16{} : s[i & 1],
+                                                                  0, 0, 0);
+            }
+            if (j + PF < N) r[j % PF] = frag(j + PF);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+
+    // V phase: weights of the tile whose first key is key0, from s into p,
+    // against the running reference; if some lane's 32 weights sum to more
+    // than kSpecLimit (or are not finite: the first tile), the reference is
+    // raised to the exact running max, O and the sums are rescaled and the
+    // weights recomputed.  MASK: keys at or past Skv get weight exactly 0.
+    auto vphase = [&](int key0, auto mask) __attribute__((always_inline)) {
+        constexpr bool MASK = decltype(mask)::value;
+        auto valid = [&](int kb, int i) { return key0 + kb * 32 + (i >> 2) * 8 + hi * 4 + (i & 3) < Skv; };
+        float e_sum = 0.f, r_sum = 0.f;
+        auto weights = [&](float nm) __attribute__((always_inline)) {
+            float a0 = 0.f, a1 = 0.f, r0 = 0.f, r1 = 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 16; i += 2) {
+                    float e0 = __builtin_amdgcn_exp2f(fmaf(s[kb][i], c, nm));
+                    float e1 = __builtin_amdgcn_exp2f(fmaf(s[kb][i + 1], c, nm));
+                    if (MASK) {
+                        e0 = valid(kb, i) ? e0 : 0.f;
+                        e1 = valid(kb, i + 1) ? e1 : 0.f;
+                    }
+                    bf16x2 pk;
+                    pk[0] = (__bf16)e0;
+                    pk[1] = (__bf16)e1;
+                    p[kb * 2 + (i >> 3)][i & 7] = pk[0];
+                    p[kb * 2 + (i >> 3)][(i & 7) + 1] = pk[1];
+                    const uint32_t u = __builtin_bit_cast(uint32_t, pk);
+                    r0 += __builtin_bit_cast(float, u << 16);
+                    r1 += __builtin_bit_cast(float, u & 0xffff0000u);
+                    a0 += e0;
+                    a1 += e1;
+                }
+            e_sum = a0 + a1;
+            r_sum = r0 + r1;
+        };
+        weights(-mref);
+        const bool over = !(e_sum <= kSpecLimit);
+        if (__builtin_amdgcn_ballot_w64(over) != 0) {
+            float m0 = -INFINITY, m1 = -INFINITY;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                m0 = fmaxf(m0, (!MASK || valid(0, i)) ? s[0][i] : -INFINITY);
+                m1 = fmaxf(m1, (!MASK || valid(1, i)) ? s[1][i] : -INFINITY);
+            }
+            const float mnew = fmaxf(mref, pair_max(fmaxf(m0, m1)) * c);
+            const float alpha = __builtin_amdgcn_exp2f(mref - mnew);
+            mref = mnew;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
+            lsum *= alpha;
+            lrnd *= alpha;
+            weights(-mnew);
+        }
+        lsum += e_sum;
+        lrnd += r_sum;
+    };
+
+    using T_ = std::true_type;
+    using F_ = std::false_type;
+    auto st = [](int u) { return u & (kStagesPP - 1); };  // ring stage of the work item's tile u
+    auto key0 = [&](int u) { return (kt0 + u) * kBlockN; };
+    auto vlast = [&](int u) __attribute__((always_inline)) {  // V phase of the last (possibly ragged) tile
+        if (ragged_end)
+            vphase(key0(u), T_{});
+        else
+            vphase(key0(u), F_{});
+    };
+    // Barrier between phases.  Nothing moves across it (the compiler would
+    // otherwise hoist a V phase's register-only work above it, into the same
+    // interval as the wave's own M phase), and the score and weight registers
+    // are pinned to their side of it.
+    auto phase_barrier = [&]() __attribute__((always_inline)) {
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+        __builtin_amdgcn_sched_barrier(0);
+        __asm__ volatile("" : "+v"(s[0]), "+v"(s[1]), "+v"(p[0]), "+v"(p[1]), "+v"(p[2]), "+v"(p[3]));
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    // Prologue: tiles 0 and 1 in flight, tile 0 landed.
+    issue_next();
+    issue_next();
+    wait_vmcnt<PER_TILE>();
+    __syncthreads();
+
+    // Interval pairs u = 0..T, two barriers each (the same count in both
+    // groups).  Group 0 runs M(u) | V(u), group 1 runs V(u-1) | M(u).  Each
+    // wave copies tile u+2 right after its M(u) (stage of tile u-2, last read
+    // by PV(u-2) in pair u-1) and, before the barrier that ends pair u, waits
+    // for its copies of tile u+1, which M(u+1) reads after that barrier.  The
+    // M phase runs at raised priority.
+    if (grp == 0) {
+        __builtin_amdgcn_s_setprio(1);
+        mphase(st(0), st(0), F_{}, T_{});
+        __builtin_amdgcn_s_setprio(0);
+        issue_next();
+        phase_barrier();
+        if (T == 1)
+            vlast(0);
+        else
+            vphase(key0(0), F_{});
+        wait_vmcnt<PER_TILE>();
+        phase_barrier();
+        for (int u = 1; u < T - 1; ++u) {
+            __builtin_amdgcn_s_setprio(1);
+            mphase(st(u), st(u - 1), T_{}, T_{});
+            __builtin_amdgcn_s_setprio(0);
+            issue_next();
+            phase_barrier();
+            vphase(key0(u), F_{});
+            wait_vmcnt<PER_TILE>();
+            phase_barrier();
+        }
+        if (T >= 2) {
+            __builtin_amdgcn_s_setprio(1);
+            mphase(st(T - 1), st(T - 2), T_{}, T_{});
+            __builtin_amdgcn_s_setprio(0);
+            issue_next();
+            phase_barrier();
+            vlast(T - 1);
+            wait_vmcnt<PER_TILE>();
+            phase_barrier();
+        }
+        __builtin_amdgcn_s_setprio(1);
+        mphase(st(T), st(T - 1), T_{}, F_{});
+        __builtin_amdgcn_s_setprio(0);
+        phase_barrier();
+        phase_barrier();
+    } else {
+        phase_barrier();
+        __builtin_amdgcn_s_setprio(1);
+        mphase(st(0), st(0), F_{}, T_{});
+        __builtin_amdgcn_s_setprio(0);
+        issue_next();
+        wait_vmcnt<PER_TILE>();
+        phase_barrier();
+        for (int u = 1; u < T; ++u) {
+            vphase(key0(u - 1), F_{});
+            phase_barrier();
+            __builtin_amdgcn_s_setprio(1);
+            mphase(st(u), st(u - 1), T_{}, T_{});
+            __builtin_amdgcn_s_setprio(0);
+            issue_next();
+            wait_vmcnt<PER_TILE>();
+            phase_barrier();
+        }
+        vlast(T - 1);
+        phase_barrier();
+        __builtin_amdgcn_s_setprio(1);
+        mphase(st(T), st(T - 1), T_{}, F_{});
+        __builtin_amdgcn_s_setprio(0);
+        issue_next();
+        wait_vmcnt<PER_TILE>();
+        phase_barrier();
+    }
+    wait_vmcnt<0>();  // the clamped trailing copies must land before the workgroup exits
+
+    store_row<D, OUT_F32>(a, pl, oacc, lsum, lrnd, mref, b, h, qi, qrow, slot);
 }
 
 // Log-sum-exp combination of the key-range partials of each split tile
@@ -779,6 +1179,18 @@ hipMemPool_t workspace_pool()
     return pools[dev];
 }
 
+// REGENVC_ATTN_SCHEDULE=pingpong|interleaved forces one schedule for every
+// launch (diagnostics and tests; read at each launch); unset or anything else
+// selects by the number of key tiles.
+int forced_schedule()
+{
+    const char *e = getenv("REGENVC_ATTN_SCHEDULE");
+    if (e == nullptr) return 0;
+    if (strcmp(e, "pingpong") == 0) return 1;
+    if (strcmp(e, "interleaved") == 0) return 2;
+    return 0;
+}
+
 template <int D, bool OUT_F32>
 hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream)
 {
@@ -794,8 +1206,12 @@ hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream)
         pl.ws_o = static_cast<float *>(ws);
         pl.ws_lse = pl.ws_o + (size_t)pl.n_units * BM * D;
     }
-    hipLaunchKernelGGL((attn_fwd_kernel<D, OUT_F32>), dim3((unsigned)(pl.n_dp + pl.n_units)), dim3(kThreads), 0,
-                       stream, a, pl);
+    const dim3 grid((unsigned)(pl.n_dp + pl.n_units)), block(kThreads);
+    const int forced = forced_schedule();
+    if (forced == 1 || (forced == 0 && pl.n_kt >= kPingPongMinTiles))
+        hipLaunchKernelGGL((attn_fwd_pingpong_kernel<D, OUT_F32>), grid, block, 0, stream, a, pl);
+    else
+        hipLaunchKernelGGL((attn_fwd_kernel<D, OUT_F32>), grid, block, 0, stream, a, pl);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && pl.n_units > 0) {
         const int64_t threads = (int64_t)(pl.n_tiles - pl.n_dp) * BM * (D / 4);

@@ -168,23 +168,21 @@ def test_peaky_scores_in_the_key_loop():
                   rows=sample_rows(Sq, 200, 22))
 
 
-@pytest.mark.parametrize("D", [128, 64])
-def test_score_jumps_in_either_key_half(D):
+def score_jumps(D, n_full, name):
     """Keys built to jump the running max by more than 8 (log2 units; median
-    ~14) at chosen places: the second 32-key half of tile 2 (rescale in the
-    middle of the P V products), the first half of tile 4 (rescale before
-    them) and the ragged last tile (exact-max path).  Queries share a
-    direction u; the jump keys are multiples of u, so (nearly) every query row
-    sees each jump.  One whole query tile per CU keeps every workgroup in the
-    steady-state key loop (sampled rows)."""
-    B, H, Skv = 1, 2, 6 * 64 + 20
+    ~14) at chosen places: the second 32-key half of tile 2, the first half
+    of tile 4 and the ragged last tile (n_full whole tiles + 20 keys).
+    Queries share a direction u; the jump keys are multiples of u, so (nearly)
+    every query row sees each jump.  One whole query tile per CU keeps every
+    workgroup in the steady-state key loop (sampled rows)."""
+    B, H, Skv = 1, 2, n_full * 64 + 20
     Sq = whole_tile_rows(H)
     rng = np.random.default_rng(31)
     u = rng.standard_normal((1, 1, H, D))
     qf = rng.standard_normal((B, Sq, H, D)) + u
     kf = rng.standard_normal((B, Skv, H, D))
     g = math.sqrt(128 / D)
-    for key, mult in ((2 * 64 + 40, 1.5), (4 * 64 + 8, 2.5), (6 * 64 + 11, 3.5)):
+    for key, mult in ((2 * 64 + 40, 1.5), (4 * 64 + 8, 2.5), (n_full * 64 + 11, 3.5)):
         kf[:, key] = g * mult * u[0, 0] + 0.1 * rng.standard_normal((B, H, D))
     vf = rng.standard_normal((B, Skv, H, D))
     q, k, v = (synth.f32_to_bf16_bits(x.astype(np.float32)) for x in (qf, kf, vf))
@@ -193,7 +191,15 @@ def test_score_jumps_in_either_key_half(D):
     torch.cuda.synchronize()
     rows = sample_rows(Sq, 200, 31)
     o_ref, lse_ref = oracle.attn(np.ascontiguousarray(q[:, rows]), k, v, scale)
-    assert_close(f"score jumps d={D}", host(o)[:, rows], o_ref, lse.cpu().numpy()[:, :, rows], lse_ref)
+    assert_close(name, host(o)[:, rows], o_ref, lse.cpu().numpy()[:, :, rows], lse_ref)
+
+
+@pytest.mark.parametrize("D", [128, 64])
+def test_score_jumps_in_either_key_half(D):
+    """Seven key tiles (the interleaved schedule): the jump in the second
+    half of tile 2 rescales O in the middle of the P V products, the one in
+    tile 4 before them, the last one goes through the exact-max path."""
+    score_jumps(D, 6, f"score jumps d={D}")
 
 
 def test_zero_scale_gives_value_mean():
@@ -311,6 +317,85 @@ def test_empty_query_set_is_a_no_op():
     o, lse = api().attn_fwd(dev(q), dev(k), dev(v))
     torch.cuda.synchronize()
     assert o.numel() == 0 and lse.numel() == 0
+
+
+# ------------------------------------------------------------------ both schedules
+# Launches with many key tiles run the ping-pong schedule, short ones the
+# interleaved one; REGENVC_ATTN_SCHEDULE forces either, so that each is
+# checked on every case below whatever its length.
+SCHEDULES = ["interleaved", "pingpong"]
+
+
+@pytest.fixture(params=SCHEDULES)
+def schedule(request, monkeypatch):
+    monkeypatch.setenv("REGENVC_ATTN_SCHEDULE", request.param)
+    return request.param
+
+
+@pytest.mark.parametrize("Sq,Skv,D,out", [
+    (1, 1, 128, "f32"), (65, 127, 128, "bf16"), (255, 257, 64, "bf16"), (300, 1000, 128, "f32"),
+    (513, 1, 64, "bf16"), (257, 2730, 128, "f32")])
+def test_schedule_ragged_shapes(schedule, Sq, Skv, D, out):
+    dt = torch.float32 if out == "f32" else torch.bfloat16
+    run_and_check(f"{schedule} Sq={Sq} Skv={Skv} D={D} {out}", 2, 2, Sq, Skv, D, 200 + Sq + Skv, dt)
+
+
+def test_schedule_peaky_key_loop(schedule):
+    """Peaky scores (scale 8/sqrt(d)) over 35 key tiles in whole-tile work
+    items: the reference moves many times inside the key loop.  fp32 output:
+    |O| reaches ~4 here, where one bf16 rounding step of the output alone is
+    up to 2^-6."""
+    H = 4
+    Sq = whole_tile_rows(H)
+    run_and_check(f"{schedule} peaky scale x8, key loop", 1, H, Sq, 35 * 64 - 7, 128, 27, torch.float32,
+                  scale=8 / math.sqrt(128), rows=sample_rows(Sq, 200, 27))
+
+
+@pytest.mark.parametrize("D", [128, 64])
+def test_schedule_score_jumps(schedule, D):
+    """Score jumps (tiles 2, 4 and the ragged last of 34) under each schedule."""
+    score_jumps(D, 33, f"{schedule} score jumps d={D}, 34 tiles")
+
+
+def test_schedule_wide_key_value_strides(schedule):
+    """K/V rows 2^24 + 8 elements apart: every tile copy takes the 64-bit
+    address path; bitwise equal to contiguous K/V under the same schedule."""
+    H, D, Skv = 2, 128, 70
+    Sq = whole_tile_rows(H)
+    q, k, v = synth.qkv(33, 1, H, Sq, Skv, D)
+    S = (1 << 24) + 8
+    wide = []
+    for x in (k, v):
+        buf = torch.empty((Skv - 1) * S + H * D, dtype=torch.bfloat16, device="cuda")
+        view = buf.as_strided((1, Skv, H, D), (Skv * S, S, D, 1))
+        view.copy_(dev(x))
+        wide.append(view)
+    scale = synth.default_scale(D)
+    o_w, l_w = api().attn_fwd(dev(q), wide[0], wide[1], scale=scale, out_dtype=torch.float32)
+    o_c, l_c = api().attn_fwd(dev(q), dev(k), dev(v), scale=scale, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert torch.equal(o_w, o_c) and torch.equal(l_w, l_c)
+    rows = sample_rows(Sq, 100, 33)
+    o_ref, l_ref = oracle.attn(np.ascontiguousarray(q[:, rows]), k, v, scale)
+    assert_close(f"{schedule} K/V rows 2^24 + 8 apart", host(o_w)[:, rows], o_ref, l_w.cpu().numpy()[:, :, rows],
+                 l_ref)
+    del wide
+
+
+def test_schedule_window_rows(schedule):
+    """The window shape (12 heads x 10920 tokens, split tiles included) under
+    each schedule, on the rows of the last query tile of two heads."""
+    B, H, S, D = 1, 12, 10920, 128
+    q, k, v = synth.qkv(3, B, H, S, S, D)
+    o, lse = api().attn_fwd(dev(q), dev(k), dev(v))
+    torch.cuda.synchronize()
+    rows = np.arange(S - 300, S)
+    for hh in (0, 11):
+        o_ref, l_ref = oracle.attn(np.ascontiguousarray(q[:, rows][:, :, hh:hh + 1]),
+                                   np.ascontiguousarray(k[:, :, hh:hh + 1]), np.ascontiguousarray(v[:, :, hh:hh + 1]),
+                                   synth.default_scale(D))
+        assert_close(f"{schedule} window head {hh} last rows", host(o)[:, rows][:, :, hh:hh + 1], o_ref,
+                     lse.cpu().numpy()[:, hh:hh + 1][:, :, rows], l_ref)
 
 
 # ------------------------------------------------------------------ partial + merge
