@@ -223,7 +223,7 @@ def main():
     roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": achieved / PEAK_BF16_TFLOPS,
                 "traffic": measured_traffic() if dom == "self" else None,
-                "kernel": "regenvc_attn_fwd: attn_fwd_kernel + split_fixup_kernel" if dom == "self"
+                "kernel": "regenvc_attn_fwd: attn_fwd_pingpong_kernel + split_fixup_kernel" if dom == "self"
                 else f"attention ({dom})"}
 
     line = {
