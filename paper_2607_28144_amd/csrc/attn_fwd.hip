@@ -909,8 +909,13 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
                     pk[1] = (__bf16)e1;
                     p[kb * 2 + (i >> 3)][i & 7] = pk[0];
                     p[kb * 2 + (i >> 3)][(i & 7) + 1] = pk[1];
+                    // the two rounded weights back in fp32: shift / mask the
+                    // packed pair (as asm: the compiler would otherwise round
+                    // e0 again with a second conversion instead of shifting)
                     const uint32_t u = __builtin_bit_cast(uint32_t, pk);
-                    r0 += __builtin_bit_cast(float, u << 16);
+                    uint32_t lo;
+                    __asm__("v_lshlrev_b32 %0, 16, %1" : "=v"(lo) : "v"(u));
+                    r0 += __builtin_bit_cast(float, lo);
                     r1 += __builtin_bit_cast(float, u & 0xffff0000u);
                     a0 += e0;
                     a1 += e1;
