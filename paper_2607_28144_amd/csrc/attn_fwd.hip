@@ -147,7 +147,7 @@ __device__ __forceinline__ void lds_dma16_s(const void *gbase, uint32_t off, uin
 template <int LOADS>
 __device__ __forceinline__ void lds_dma16_group(const uint16_t *base, const uint32_t (&off)[LOADS], uint32_t lds_base)
 {
-    const char *b = reinterpret_cast<const char *>(base);
+    const uint64_t b = (uint64_t)(uintptr_t)base;  // integer arithmetic: b - 1024 may precede the tensor
     if constexpr (LOADS == 1) {
         __asm__ volatile("s_nop 4\n\ts_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
                          :
