@@ -185,22 +185,15 @@ __device__ __forceinline__ float pair_sum(float x)
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Stores the bf16 pair (x0, x1) as weights j, j+1 of a P operand and adds
-// the two rounded values (as the P V product sees them) to r.  O is divided
-// by the sum of these rounded weights, so that it is a convex combination of
-// V rows with exactly the weights the MFMA used: a dominant key then returns
-// its V row without the up-to-2^-9 error of its own weight's rounding.  (A
-// dot2 against (1, 1) is one instruction per pair; unpacking the pair costs
-// four.)
-__device__ __forceinline__ void put_pair(bf16x8 &dst, int j, float x0, float x1, float &r)
+// Stores the weights (x0, x1), rounded to bf16 (nearest even, one packed
+// conversion), as weights j, j+1 of a P operand.
+__device__ __forceinline__ void put_pair(bf16x8 &dst, int j, float x0, float x1)
 {
     bf16x2 pk;
     pk[0] = (__bf16)x0;
     pk[1] = (__bf16)x1;
     dst[j] = pk[0];
     dst[j + 1] = pk[1];
-    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-    r = __builtin_amdgcn_fdot2_f32_bf16(pk, ones, r, false);
 }
 
 // Online-softmax step for one 32-query block over one 64-key tile.
@@ -210,16 +203,14 @@ __device__ __forceinline__ void put_pair(bf16x8 &dst, int j, float x0, float x1,
 //   c      : scale * log2(e)
 //   mref   : exponent reference (log2 units), raised lazily
 //   lsum   : running fp32 sum of exp2(s*c - mref) over this lane's keys (the
-//            unrounded weights, for LSE: summing the bf16-rounded ones would
-//            move LSE by up to 2^-9 when few keys dominate)
-//   lrnd   : the same sum of the bf16-rounded weights (normalizes O)
+//            unrounded weights; it normalizes O and gives LSE)
 //   p      : bf16 P^T operands of the four 16-key MFMA steps of the tile
 //   alpha  : factor the O accumulator must be multiplied by (1 if unchanged)
 //   upd    : wave-uniform flag: some lane raised its reference
 // MASK: keys at or past Skv (only in the last tile) get weight exactly 0.
 template <bool MASK>
-__device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, float &mref, float &lsum, float &lrnd,
-                                              bf16x8 (&p)[4], float &alpha, bool &upd, int key0, int Skv)
+__device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, float &mref, float &lsum, bf16x8 (&p)[4],
+                                              float &alpha, bool &upd, int key0, int Skv)
 {
     const int hi = (threadIdx.x >> 5) & 1;
     auto valid = [&](int kb, int i) { return key0 + kb * 32 + (i >> 2) * 8 + hi * 4 + (i & 3) < Skv; };
@@ -235,7 +226,7 @@ __device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, flo
     alpha = __builtin_amdgcn_exp2f(mref - mnew);
     mref = mnew;
     const float nm = -mnew;
-    float acc0 = 0.f, acc1 = 0.f, accr = 0.f;
+    float acc0 = 0.f, acc1 = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -246,12 +237,11 @@ __device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, flo
                 e0 = valid(kb, i) ? e0 : 0.f;
                 e1 = valid(kb, i + 1) ? e1 : 0.f;
             }
-            put_pair(p[kb * 2 + (i >> 3)], i & 7, e0, e1, accr);
+            put_pair(p[kb * 2 + (i >> 3)], i & 7, e0, e1);
             acc0 += e0;
             acc1 += e1;
         }
     lsum = fmaf(lsum, alpha, acc0 + acc1);
-    lrnd = fmaf(lrnd, alpha, accr);
 }
 
 // Work item of a workgroup: one key range of a split tile (the first
@@ -283,20 +273,19 @@ __device__ __forceinline__ WorkItem work_item(const AttnPlan &pl, int item)
     return w;
 }
 
-// Epilogue of one lane's query row: O = O^T / l with l the sum of the
-// bf16-rounded weights (the ones the P V products used), LSE = ln2 * (m_ref +
-// log2 l') with l' the sum of the exact weights; a split tile's key range
-// writes its normalized partial to the workspace instead.  lsum, lrnd are
-// this lane's halves (the other half is in lane^32).
+// Epilogue of one lane's query row: O = O^T / l and LSE = ln2 * (m_ref +
+// log2 l), with l the fp32 sum of the weights; a split tile's key range
+// writes its normalized partial to the workspace instead.  lsum is this
+// lane's half of l (the other half is in lane^32).
 template <int D, bool OUT_F32>
 __device__ __forceinline__ void store_row(const AttnArgs &a, const AttnPlan &pl, const f32x16 (&oacc)[D / 32],
-                                          float lsum, float lrnd, float mref, int b, int h, int qi, int qrow, int slot)
+                                          float lsum, float mref, int b, int h, int qi, int qrow, int slot)
 {
     constexpr int BM = kWaves * 32;
     constexpr int DB = D / 32;
     const int hi = (threadIdx.x >> 5) & 1;
     const float lt = pair_sum(lsum);
-    const float inv = 1.0f / pair_sum(lrnd);
+    const float inv = 1.0f / lt;
     const float lse_val = (mref + __log2f(lt)) * kLn2;
     if (qi >= a.Sq) return;
     if (slot >= 0) {
@@ -490,15 +479,14 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 
     const float c = a.scale * kLog2e;
     float mref = -INFINITY;
-    float lsum = 0.f, lrnd = 0.f;
+    float lsum = 0.f;
     f32x16 scur[2], snext[2];
     bf16x8 p[4];
     float alpha = 1.f;
     bool upd = false;
     // softmax state carried from phase X into phase Y of a step: -mref, the
-    // first half's weight sum, the second half's partial sums, and the sums
-    // of the rounded weights of both halves
-    float nm = 0.f, acc0 = 0.f, acc1 = 0.f, acc2 = 0.f, rh1 = 0.f, rh2 = 0.f;
+    // first half's weight sum and the second half's partial sums
+    float nm = 0.f, acc0 = 0.f, acc1 = 0.f, acc2 = 0.f;
 
     // O^T += V^T P^T for the key tile in stage `st`: each MFMA's V fragment is read PF
     // MFMAs ahead; the order is pinned so that the waits stay PF deep.  With
@@ -523,7 +511,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
                     for (int e = i * TN; e < (i + 1) * TN; e += 2) {
                         const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[1][e], c, nm));
                         const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[1][e + 1], c, nm));
-                        put_pair(p[2 + (e >> 3)], e & 7, x0, x1, rh2);
+                        put_pair(p[2 + (e >> 3)], e & 7, x0, x1);
                         acc1 += x0;
                         acc2 += x1;
                     }
@@ -545,22 +533,19 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 #pragma unroll
                         for (int db = 0; db < DB; ++db) oacc[db] *= al;
                         lsum *= al;
-                        lrnd *= al;
                         acc0 *= al;
-                        rh1 *= al;
-                        acc1 = acc2 = rh2 = 0.f;
+                        acc1 = acc2 = 0.f;
 #pragma unroll
                         for (int e = 0; e < 16; e += 2) {
                             const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[1][e], c, -mnew));
                             const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[1][e + 1], c, -mnew));
-                            put_pair(p[2 + (e >> 3)], e & 7, x0, x1, rh2);
+                            put_pair(p[2 + (e >> 3)], e & 7, x0, x1);
                             acc1 += x0;
                             acc2 += x1;
                         }
                         a2 = acc1 + acc2;
                     }
                     lsum += acc0 + a2;
-                    lrnd += rh1 + rh2;
                 }
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -585,7 +570,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         __builtin_amdgcn_s_setprio(1);
         constexpr int STRIDE = NK / 8;
         bf16x8 kr[PF];
-        acc0 = acc1 = rh1 = 0.f;
+        acc0 = acc1 = 0.f;
         const float nm0 = -mref;
 #pragma unroll
         for (int i = 0; i < PF; ++i) kr[i] = kfrag(kt, i);
@@ -601,7 +586,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
                 const int e = 2 * (i / STRIDE);
                 const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[0][e], c, nm0));
                 const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[0][e + 1], c, nm0));
-                put_pair(p[e >> 3], e & 7, x0, x1, rh1);
+                put_pair(p[e >> 3], e & 7, x0, x1);
                 acc0 += x0;
                 acc1 += x1;
             }
@@ -610,7 +595,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         float a1 = acc0 + acc1;
         // keep this half of the softmax in this phase: without a use here the
         // compiler sinks it past the branch below, next to the P V products
-        __asm__ volatile("" : : "v"(p[0]), "v"(p[1]), "v"(a1), "v"(rh1));
+        __asm__ volatile("" : : "v"(p[0]), "v"(p[1]), "v"(a1));
         upd = __builtin_amdgcn_ballot_w64(!(a1 <= kSpecLimit) && a1 == a1) != 0;
         if (upd) {
             float m0 = -INFINITY, m1 = -INFINITY;
@@ -623,20 +608,19 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
             alpha = __builtin_amdgcn_exp2f(mref - mnew);
             mref = mnew;
             lsum *= alpha;
-            lrnd *= alpha;
-            acc0 = acc1 = rh1 = 0.f;
+            acc0 = acc1 = 0.f;
 #pragma unroll
             for (int e = 0; e < 16; e += 2) {
                 const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[0][e], c, -mnew));
                 const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[0][e + 1], c, -mnew));
-                put_pair(p[e >> 3], e & 7, x0, x1, rh1);
+                put_pair(p[e >> 3], e & 7, x0, x1);
                 acc0 += x0;
                 acc1 += x1;
             }
             a1 = acc0 + acc1;
         }
         acc0 = a1;
-        acc1 = acc2 = rh2 = 0.f;
+        acc1 = acc2 = 0.f;
         nm = -mref;
     };
 
@@ -670,7 +654,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
             issue_next(next_stage(st1));             // tile t+kAhead, into the stage tile t-1 used
             qk_softmax(st1, sc, sn);
         } else {
-            softmax_block<MASK>(sc, c, mref, lsum, lrnd, p, alpha, upd, t * kBlockN, Skv);
+            softmax_block<MASK>(sc, c, mref, lsum, p, alpha, upd, t * kBlockN, Skv);
         }
         // ---- O rescale (rare), outside the MFMA streams
         if (upd) {
@@ -707,7 +691,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         step(t, scur, snext, F_{}, F_{});
     wait_vmcnt<0>();  // the clamped trailing copies must land before the workgroup exits
 
-    store_row<D, OUT_F32>(a, pl, oacc, lsum, lrnd, mref, b, h, qi, qrow, slot);
+    store_row<D, OUT_F32>(a, pl, oacc, lsum, mref, b, h, qi, qrow, slot);
 }
 
 // Ping-pong schedule of the same computation (launches with many key tiles).
@@ -721,13 +705,15 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 // its own weights with its MFMAs keeps the matrix pipe about half busy; two
 // waves in opposite phases keep it about 80 % busy in a probe of the same
 // instruction mix.)  Tiles go through a 4-stage LDS ring: each wave copies its
-// share of tile u+2 right after M(u), into the stage of tile u-2.
+// share of tile u+2 right after M(u), into the stage of tile u-2.  A wave
+// reads the first PF operand fragments of its next M phase (V fragments of a
+// tile that landed a pair earlier) before the barrier that starts the phase,
+// so their LDS latency passes while it waits there rather than before its
+// first MFMA.
 //
 // Weights use the speculative reference of the interleaved kernel, checked
 // once per tile (a lane's 32 weights summing to more than kSpecLimit), and
-// the same two running sums; the sum of the bf16-rounded weights is formed by
-// unpacking the pairs (the dot2 instructions would occupy the matrix pipe the
-// other wave is streaming on).
+// the same running sum.
 template <int D, bool OUT_F32>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
@@ -853,11 +839,21 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     f32x16 s[2];
     bf16x8 p[4];
     const float c = a.scale * kLog2e;
-    float mref = -INFINITY, lsum = 0.f, lrnd = 0.f;
+    float mref = -INFINITY, lsum = 0.f;
+
+    // First PF operand fragments of an M phase (see mphase), read ahead of it.
+    bf16x8 r[PF];
+    auto mprefetch = [&](int stq, int stv, auto do_pv) __attribute__((always_inline)) {
+        constexpr int N0 = decltype(do_pv)::value ? NV : 0;
+        const lds_char *vt = stage_ptr(stv);
+        const lds_char *kt = stage_ptr(stq);
+#pragma unroll
+        for (int j = 0; j < PF; ++j) r[j] = j < N0 ? vfrag(vt, j) : kfrag(kt, j - N0);
+    };
 
     // M phase: PV of the tile in stage stv (weights p), then QK of the tile in
     // stage stq (into s); the order is pinned so the fragment reads stay PF
-    // MFMAs ahead.
+    // MFMAs ahead.  The first PF fragments are in r (mprefetch, same stages).
     auto mphase = [&](int stq, int stv, auto do_pv, auto do_qk) __attribute__((always_inline)) {
         constexpr bool PV = decltype(do_pv)::value, QK = decltype(do_qk)::value;
         constexpr int N0 = PV ? NV : 0;
@@ -865,9 +861,6 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
         const lds_char *vt = stage_ptr(stv);
         const lds_char *kt = stage_ptr(stq);
         auto frag = [&](int j) -> bf16x8 { return j < N0 ? vfrag(vt, j) : kfrag(kt, j - N0); };
-        bf16x8 r[PF];
-#pragma unroll
-        for (int j = 0; j < PF; ++j) r[j] = frag(j);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int j = 0; j < N; ++j) {
@@ -886,14 +879,15 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     // V phase: weights of the tile whose first key is key0, from s into p,
     // against the running reference; if some lane's 32 weights sum to more
     // than kSpecLimit (or are not finite: the first tile), the reference is
-    // raised to the exact running max, O and the sums are rescaled and the
+    // raised to the exact running max, O and the sum are rescaled and the
     // weights recomputed.  MASK: keys at or past Skv get weight exactly 0.
     auto vphase = [&](int key0, auto mask) __attribute__((always_inline)) {
         constexpr bool MASK = decltype(mask)::value;
         auto valid = [&](int kb, int i) { return key0 + kb * 32 + (i >> 2) * 8 + hi * 4 + (i & 3) < Skv; };
-        float e_sum = 0.f, r_sum = 0.f;
+        float e_sum = 0.f;
         auto weights = [&](float nm) __attribute__((always_inline)) {
-            float a0 = 0.f, a1 = 0.f, r0 = 0.f, r1 = 0.f;
+            // -0 starts the sums (0 + x is not foldable: it turns -0 into +0)
+            float a0 = -0.f, a1 = -0.f;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -904,24 +898,11 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
                         e0 = valid(kb, i) ? e0 : 0.f;
                         e1 = valid(kb, i + 1) ? e1 : 0.f;
                     }
-                    bf16x2 pk;
-                    pk[0] = (__bf16)e0;
-                    pk[1] = (__bf16)e1;
-                    p[kb * 2 + (i >> 3)][i & 7] = pk[0];
-                    p[kb * 2 + (i >> 3)][(i & 7) + 1] = pk[1];
-                    // the two rounded weights back in fp32: shift / mask the
-                    // packed pair (as asm: the compiler would otherwise round
-                    // e0 again with a second conversion instead of shifting)
-                    const uint32_t u = __builtin_bit_cast(uint32_t, pk);
-                    uint32_t lo;
-                    __asm__("v_lshlrev_b32 %0, 16, %1" : "=v"(lo) : "v"(u));
-                    r0 += __builtin_bit_cast(float, lo);
-                    r1 += __builtin_bit_cast(float, u & 0xffff0000u);
+                    put_pair(p[kb * 2 + (i >> 3)], i & 7, e0, e1);
                     a0 += e0;
                     a1 += e1;
                 }
             e_sum = a0 + a1;
-            r_sum = r0 + r1;
         };
         weights(-mref);
         const bool over = !(e_sum <= kSpecLimit);
@@ -938,11 +919,9 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
 #pragma unroll
             for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
             lsum *= alpha;
-            lrnd *= alpha;
             weights(-mnew);
         }
         lsum += e_sum;
-        lrnd += r_sum;
     };
 
     using T_ = std::true_type;
@@ -978,8 +957,11 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     // wave copies tile u+2 right after its M(u) (stage of tile u-2, last read
     // by PV(u-2) in pair u-1) and, before the barrier that ends pair u, waits
     // for its copies of tile u+1, which M(u+1) reads after that barrier.  The
-    // M phase runs at raised priority.
+    // fragments an M phase starts with are read before the barrier ahead of
+    // it: V fragments of its tile u-1, which landed a pair earlier and is not
+    // overwritten before pair u+1.  The M phase runs at raised priority.
     if (grp == 0) {
+        mprefetch(st(0), st(0), F_{});
         __builtin_amdgcn_s_setprio(1);
         mphase(st(0), st(0), F_{}, T_{});
         __builtin_amdgcn_s_setprio(0);
@@ -990,6 +972,7 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
         else
             vphase(key0(0), F_{});
         wait_vmcnt<PER_TILE>();
+        mprefetch(st(1), st(0), T_{});
         phase_barrier();
         for (int u = 1; u < T - 1; ++u) {
             __builtin_amdgcn_s_setprio(1);
@@ -999,6 +982,7 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
             phase_barrier();
             vphase(key0(u), F_{});
             wait_vmcnt<PER_TILE>();
+            mprefetch(st(u + 1), st(u), T_{});
             phase_barrier();
         }
         if (T >= 2) {
@@ -1009,6 +993,7 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
             phase_barrier();
             vlast(T - 1);
             wait_vmcnt<PER_TILE>();
+            mprefetch(st(T), st(T - 1), T_{});
             phase_barrier();
         }
         __builtin_amdgcn_s_setprio(1);
@@ -1017,6 +1002,7 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
         phase_barrier();
         phase_barrier();
     } else {
+        mprefetch(st(0), st(0), F_{});
         phase_barrier();
         __builtin_amdgcn_s_setprio(1);
         mphase(st(0), st(0), F_{}, T_{});
@@ -1026,6 +1012,7 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
         phase_barrier();
         for (int u = 1; u < T; ++u) {
             vphase(key0(u - 1), F_{});
+            mprefetch(st(u), st(u - 1), T_{});
             phase_barrier();
             __builtin_amdgcn_s_setprio(1);
             mphase(st(u), st(u - 1), T_{}, T_{});
@@ -1035,6 +1022,7 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
             phase_barrier();
         }
         vlast(T - 1);
+        mprefetch(st(T), st(T - 1), T_{});
         phase_barrier();
         __builtin_amdgcn_s_setprio(1);
         mphase(st(T), st(T - 1), T_{}, F_{});
@@ -1045,7 +1033,7 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     }
     wait_vmcnt<0>();  // the clamped trailing copies must land before the workgroup exits
 
-    store_row<D, OUT_F32>(a, pl, oacc, lsum, lrnd, mref, b, h, qi, qrow, slot);
+    store_row<D, OUT_F32>(a, pl, oacc, lsum, mref, b, h, qi, qrow, slot);
 }
 
 // Log-sum-exp combination of the key-range partials of each split tile
