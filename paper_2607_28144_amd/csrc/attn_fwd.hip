@@ -17,7 +17,8 @@
 //   Workgroups are renumbered so that the tiles of one head run on the same
 //   XCD (each XCD has its own L2; the hardware deals workgroups round-robin).
 //
-// Layout trick: scores are computed transposed, S^T = K Q^T, with
+// Layout trick (interleaved kernel; the ping-pong kernel uses the 16x16x32
+//   form, see there): scores are computed transposed, S^T = K Q^T, with
 //   v_mfma_f32_32x32x16_bf16 (A = 32 keys x 16 dims from LDS, B = 16 dims x
 //   32 queries held in registers).  In the 32x32 accumulator a lane owns ONE
 //   query column and 16 of the 32 keys, so row max / row sum are in-register
@@ -183,6 +184,22 @@ __device__ __forceinline__ float pair_sum(float x)
 {
     auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// x combined over the four lanes l, l^16, l^32, l^48 (each gets the result).
+__device__ __forceinline__ float quad_max(float x)
+{
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    const float t = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    auto u = __builtin_amdgcn_permlane32_swap(__float_as_uint(t), __float_as_uint(t), false, false);
+    return fmaxf(__uint_as_float(u[0]), __uint_as_float(u[1]));
+}
+__device__ __forceinline__ float quad_sum(float x)
+{
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    const float t = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    auto u = __builtin_amdgcn_permlane32_swap(__float_as_uint(t), __float_as_uint(t), false, false);
+    return __uint_as_float(u[0]) + __uint_as_float(u[1]);
 }
 
 // Stores the weights (x0, x1), rounded to bf16 (nearest even, one packed
@@ -711,26 +728,39 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 // so their LDS latency passes while it waits there rather than before its
 // first MFMA.
 //
+// The products use v_mfma_f32_16x16x32_bf16 rather than the 32x32x16 form
+// of the interleaved kernel: the same FLOPs at the same issue rate, but half
+// the accumulator bytes read and written per FLOP.  The chip runs this load
+// at its power limit, and a pure MFMA stream of the 16x16x32 form holds a
+// ~15 % higher shader clock than one of the 32x32x16 form.  Layout: a lane
+// (group g = lane/16, column x = lane%16) holds queries x and 16 + x of the
+// wave's 32, each with keys 4g .. 4g+3 of every 16-key block of S^T; row
+// sums and maxima are in-lane over those keys plus an exchange across the
+// four lane groups (only at the end, and when the reference is raised).
+//
 // Weights use the speculative reference of the interleaved kernel, checked
-// once per tile (a lane's 32 weights summing to more than kSpecLimit), and
-// the same running sum.
+// once per tile (a lane's 16 weights of one query summing to more than
+// kSpecLimit), and the same running sum.
 template <int D, bool OUT_F32>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
 {
     using G = Geo<D, kStagesPP>;
-    constexpr int NCH = G::NCH, DS = G::DS, DB = G::DB, LOADS = G::LOADS;
+    constexpr int NCH = G::NCH, LOADS = G::LOADS;
+    constexpr int KS = D / 32;           // 32-dim k-steps of Q K^T
+    constexpr int DB = D / 16;           // 16-dim blocks of O^T
     constexpr int BM = kWaves * 32;
     constexpr int PER_TILE = 2 * LOADS;  // copies per thread per tile (K and V)
     static_assert(kStagesPP == 4, "tile u+2 is copied into the stage of tile u-2");
+    static_assert(kBlockN == 64, "four 16-key blocks per tile");
 
     __shared__ __attribute__((aligned(1024))) char smem[G::LDS];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
     const int grp = wave >> 2;
-    const int hi = lane >> 5;
-    const int col = lane & 31;
+    const int g = lane >> 4;   // lane group: 4 keys of each 16-key block, 4 dims of each 16-dim block
+    const int x = lane & 15;   // query column within a 16-query block
 
     const WorkItem wi = work_item(pl, blockIdx.x);
     const int tile = wi.tile, kt0 = wi.kt0, kt1 = wi.kt1, slot = wi.slot;
@@ -738,8 +768,9 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     const int bh = tile / pl.n_qtiles;
     const int h = bh % a.H;
     const int b = bh / a.H;
-    const int qrow = wave * 32 + col;
-    const int qi = qt * BM + qrow;
+    // this lane's two queries: row wave*32 + qb*16 + x of the tile, qb = 0, 1
+    const int qrow0 = wave * 32 + x;
+    const int qi0 = qt * BM + qrow0;
 
     const uint16_t *qp = static_cast<const uint16_t *>(a.q) + b * a.q_sb + h * a.q_sh;
     const uint16_t *kp = static_cast<const uint16_t *>(a.k) + b * a.k_sb + h * a.k_sh;
@@ -748,14 +779,19 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     const int T = kt1 - kt0;  // key tiles of this work item, >= 1
     const bool ragged_end = kt1 == pl.n_kt && (Skv % kBlockN) != 0;
 
-    bf16x8 qf[DS];
+    // Q^T operand fragments (B of S^T = K Q^T): query block qb, dims
+    // 32*ks + 8*g .. +7 of query qb*16 + x.
+    bf16x8 qf[2][KS];
 #pragma unroll
-    for (int ds = 0; ds < DS; ++ds) {
-        if (qi < a.Sq)
-            qf[ds] = *reinterpret_cast<const bf16x8 *>(qp + (int64_t)qi * a.q_ss + ds * 16 + hi * 8);
-        else
-            qf[ds] = bf16x8{};
-    }
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const int qi = qi0 + qb * 16;
+            if (qi < a.Sq)
+                qf[qb][ks] = *reinterpret_cast<const bf16x8 *>(qp + (int64_t)qi * a.q_ss + ks * 32 + g * 8);
+            else
+                qf[qb][ks] = bf16x8{};
+        }
 
     // HBM -> LDS copies, as in the interleaved kernel: tiles in order kt0,
     // kt0+1, ... (one call per tile, into ring stages 0, 1, 2, ...), the last
@@ -804,42 +840,49 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
         }
     };
 
-    // Per-lane LDS byte offsets of the MFMA operand fragments (stage 0), as
-    // in the interleaved kernel.
-    int koff[DS];
+    // Per-lane LDS byte offsets of the MFMA operand fragments (stage 0).
+    // K fragment (kb, ks): key kb*16 + x, dims 32*ks + 8*g .. +7 (one 16-byte
+    // chunk; the key block is an immediate offset, the swizzle depends on
+    // the key only through x).  V^T fragment (db, ks): dim db*16 + x of keys
+    // 32*ks + 4*g .. +3 and 32*ks + 16 + 4*g .. +3, two transposing 8-byte
+    // reads in which lane x of each 16-lane group supplies key 4*g + x/4,
+    // dims db*16 + 4*(x%4) .. +3 and receives the column of dim db*16 + x.
+    // That key order is the one the S^T accumulators give the P operand.
+    int koff[KS];
 #pragma unroll
-    for (int ds = 0; ds < DS; ++ds) koff[ds] = (col * D + k_slot<NCH>(col, ds * 2 + hi) * 8) * 2;
-    const int g = lane >> 4, x = lane & 15;
+    for (int ks = 0; ks < KS; ++ks) koff[ks] = (x * D + k_slot<NCH>(x, ks * 4 + g) * 8) * 2;
     int voff[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-        const int row = 4 * (g >> 1) + (x >> 2);
-        const int dcol = db * 32 + 16 * (g & 1) + 4 * (x & 3);
+        const int row = 4 * g + (x >> 2);
+        const int dcol = db * 16 + 4 * (x & 3);
         voff[db] = G::TILE + (row * D + v_slot<NCH>(row, dcol >> 3) * 8 + (dcol & 7)) * 2;
     }
-    constexpr int NK = 2 * DS;  // K fragments (MFMAs) per tile for S^T
-    constexpr int NV = 4 * DB;  // V fragments (MFMAs) per tile for O^T
-    constexpr int PF = 4;       // fragments read ahead of their MFMA
+    constexpr int NK = 4 * KS;  // K fragments per tile (each feeds two MFMAs)
+    constexpr int NV = 2 * DB;  // V^T fragments per tile (each feeds two MFMAs)
+    constexpr int PF = 4;       // fragments read ahead of their MFMAs
     static_assert(NK >= PF && NV >= PF, "schedule assumes d >= 64");
-    auto kfrag = [&](const lds_char *kt, int i) -> bf16x8 {
-        return *(const lds_bf16x8 *)(kt + koff[i >> 1] + (i & 1) * 32 * D * 2);
+    auto kfrag = [&](const lds_char *kt, int i) -> bf16x8 {  // i = ks*4 + kb
+        return *(const lds_bf16x8 *)(kt + koff[i >> 2] + (i & 3) * 16 * D * 2);
     };
-    auto vfrag = [&](const lds_char *vt, int i) -> bf16x8 {
-        const int kk = i / DB, db = i % DB;
-        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(vt + voff[db] + kk * 16 * D * 2));
+    auto vfrag = [&](const lds_char *vt, int i) -> bf16x8 {  // i = ks*DB + db
+        const int ks = i / DB, db = i % DB;
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(vt + voff[db] + ks * 32 * D * 2));
         const bf16x4 up =
-            __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(vt + voff[db] + (kk * 16 + 8) * D * 2));
+            __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(vt + voff[db] + (ks * 32 + 16) * D * 2));
         return bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
     };
     auto stage_ptr = [&](int st) { return (const lds_char *)(smem + st * G::STAGE); };
 
-    f32x16 oacc[DB];
+    // Accumulators: oacc[db][qb] = O^T dims db*16 + 4*g .. +3 of query
+    // qb*16 + x; s[kb][qb] = S^T keys kb*16 + 4*g .. +3 of that query.
+    f32x4 oacc[DB][2];
 #pragma unroll
-    for (int db = 0; db < DB; ++db) oacc[db] = f32x16{};
-    f32x16 s[2];
-    bf16x8 p[4];
+    for (int db = 0; db < DB; ++db) oacc[db][0] = oacc[db][1] = f32x4{};
+    f32x4 s[4][2];
+    bf16x8 p[2][2];  // P^T operands: 32-key step ks, query block qb
     const float c = a.scale * kLog2e;
-    float mref = -INFINITY, lsum = 0.f;
+    float mref[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f};
 
     // First PF operand fragments of an M phase (see mphase), read ahead of it.
     bf16x8 r[PF];
@@ -852,8 +895,9 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     };
 
     // M phase: PV of the tile in stage stv (weights p), then QK of the tile in
-    // stage stq (into s); the order is pinned so the fragment reads stay PF
-    // MFMAs ahead.  The first PF fragments are in r (mprefetch, same stages).
+    // stage stq (into s); every fragment feeds the MFMAs of both query blocks;
+    // the order is pinned so the fragment reads stay PF fragments ahead.  The
+    // first PF fragments are in r (mprefetch, same stages).
     auto mphase = [&](int stq, int stv, auto do_pv, auto do_qk) __attribute__((always_inline)) {
         constexpr bool PV = decltype(do_pv)::value, QK = decltype(do_qk)::value;
         constexpr int N0 = PV ? NV : 0;
@@ -865,11 +909,16 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
 #pragma unroll
         for (int j = 0; j < N; ++j) {
             if (j < N0) {
-                oacc[j % DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(r[j % PF], p[j / DB], oacc[j % DB], 0, 0, 0);
+                const int ks = j / DB, db = j % DB;
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb)
+                    oacc[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(r[j % PF], p[ks][qb], oacc[db][qb], 0, 0, 0);
             } else {
-                const int i = j - N0;
-                s[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(r[j % PF], qf[i >> 1], i < 2 ? f32x16{} : s[i & 1],
-                                                                  0, 0, 0);
+                const int i = j - N0, ks = i >> 2, kb = i & 3;
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb)
+                    s[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(r[j % PF], qf[qb][ks],
+                                                                       ks == 0 ? f32x4{} : s[kb][qb], 0, 0, 0);
             }
             if (j + PF < N) r[j % PF] = frag(j + PF);
             __builtin_amdgcn_sched_barrier(0);
@@ -877,51 +926,62 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     };
 
     // V phase: weights of the tile whose first key is key0, from s into p,
-    // against the running reference; if some lane's 32 weights sum to more
-    // than kSpecLimit (or are not finite: the first tile), the reference is
-    // raised to the exact running max, O and the sum are rescaled and the
-    // weights recomputed.  MASK: keys at or past Skv get weight exactly 0.
+    // against the running references; if some lane's 16 weights of one of
+    // its queries sum to more than kSpecLimit (or are not finite: the first
+    // tile), the references are raised to the exact running maxima (over the
+    // four lanes that hold a query's keys), O and the sums are rescaled and
+    // the weights recomputed.  MASK: keys at or past Skv get weight exactly 0.
     auto vphase = [&](int key0, auto mask) __attribute__((always_inline)) {
         constexpr bool MASK = decltype(mask)::value;
-        auto valid = [&](int kb, int i) { return key0 + kb * 32 + (i >> 2) * 8 + hi * 4 + (i & 3) < Skv; };
-        float e_sum = 0.f;
-        auto weights = [&](float nm) __attribute__((always_inline)) {
-            // -0 starts the sums (0 + x is not foldable: it turns -0 into +0)
-            float a0 = -0.f, a1 = -0.f;
+        auto valid = [&](int kb, int i) { return key0 + kb * 16 + g * 4 + i < Skv; };
+        float e_sum[2];
+        auto weights = [&]() __attribute__((always_inline)) {
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
+            for (int qb = 0; qb < 2; ++qb) {
+                const float nm = -mref[qb];
+                // -0 starts the sums (0 + x is not foldable: it turns -0 into +0)
+                float a0 = -0.f, a1 = -0.f;
 #pragma unroll
-                for (int i = 0; i < 16; i += 2) {
-                    float e0 = __builtin_amdgcn_exp2f(fmaf(s[kb][i], c, nm));
-                    float e1 = __builtin_amdgcn_exp2f(fmaf(s[kb][i + 1], c, nm));
-                    if (MASK) {
-                        e0 = valid(kb, i) ? e0 : 0.f;
-                        e1 = valid(kb, i + 1) ? e1 : 0.f;
+                for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 4; i += 2) {
+                        float e0 = __builtin_amdgcn_exp2f(fmaf(s[kb][qb][i], c, nm));
+                        float e1 = __builtin_amdgcn_exp2f(fmaf(s[kb][qb][i + 1], c, nm));
+                        if (MASK) {
+                            e0 = valid(kb, i) ? e0 : 0.f;
+                            e1 = valid(kb, i + 1) ? e1 : 0.f;
+                        }
+                        put_pair(p[kb >> 1][qb], (kb & 1) * 4 + i, e0, e1);
+                        a0 += e0;
+                        a1 += e1;
                     }
-                    put_pair(p[kb * 2 + (i >> 3)], i & 7, e0, e1);
-                    a0 += e0;
-                    a1 += e1;
-                }
-            e_sum = a0 + a1;
-        };
-        weights(-mref);
-        const bool over = !(e_sum <= kSpecLimit);
-        if (__builtin_amdgcn_ballot_w64(over) != 0) {
-            float m0 = -INFINITY, m1 = -INFINITY;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                m0 = fmaxf(m0, (!MASK || valid(0, i)) ? s[0][i] : -INFINITY);
-                m1 = fmaxf(m1, (!MASK || valid(1, i)) ? s[1][i] : -INFINITY);
+                e_sum[qb] = a0 + a1;
             }
-            const float mnew = fmaxf(mref, pair_max(fmaxf(m0, m1)) * c);
-            const float alpha = __builtin_amdgcn_exp2f(mref - mnew);
-            mref = mnew;
+        };
+        weights();
+        const bool over = !(e_sum[0] <= kSpecLimit) || !(e_sum[1] <= kSpecLimit);
+        if (__builtin_amdgcn_ballot_w64(over) != 0) {
 #pragma unroll
-            for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
-            lsum *= alpha;
-            weights(-mnew);
+            for (int qb = 0; qb < 2; ++qb) {
+                float m0 = -INFINITY, m1 = -INFINITY;
+#pragma unroll
+                for (int kb = 0; kb < 4; kb += 2)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        m0 = fmaxf(m0, (!MASK || valid(kb, i)) ? s[kb][qb][i] : -INFINITY);
+                        m1 = fmaxf(m1, (!MASK || valid(kb + 1, i)) ? s[kb + 1][qb][i] : -INFINITY);
+                    }
+                const float mnew = fmaxf(mref[qb], quad_max(fmaxf(m0, m1)) * c);
+                const float alpha = __builtin_amdgcn_exp2f(mref[qb] - mnew);
+                mref[qb] = mnew;
+#pragma unroll
+                for (int db = 0; db < DB; ++db) oacc[db][qb] *= alpha;
+                lsum[qb] *= alpha;
+            }
+            weights();
         }
-        lsum += e_sum;
+        lsum[0] += e_sum[0];
+        lsum[1] += e_sum[1];
     };
 
     using T_ = std::true_type;
@@ -942,7 +1002,9 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
         __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
         __builtin_amdgcn_sched_barrier(0);
-        __asm__ volatile("" : "+v"(s[0]), "+v"(s[1]), "+v"(p[0]), "+v"(p[1]), "+v"(p[2]), "+v"(p[3]));
+        __asm__ volatile("" : "+v"(s[0][0]), "+v"(s[0][1]), "+v"(s[1][0]), "+v"(s[1][1]), "+v"(s[2][0]),
+                         "+v"(s[2][1]), "+v"(s[3][0]), "+v"(s[3][1]));
+        __asm__ volatile("" : "+v"(p[0][0]), "+v"(p[0][1]), "+v"(p[1][0]), "+v"(p[1][1]));
         __builtin_amdgcn_sched_barrier(0);
     };
 
@@ -1033,7 +1095,47 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     }
     wait_vmcnt<0>();  // the clamped trailing copies must land before the workgroup exits
 
-    store_row<D, OUT_F32>(a, pl, oacc, lsum, mref, b, h, qi, qrow, slot);
+    // Epilogue: per query, l = the sum of the four lanes' partial sums;
+    // O = O^T / l, LSE = ln2 * (m_ref + log2 l); a split tile's key range
+    // writes its normalized partial to the workspace instead.
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        const float lt = quad_sum(lsum[qb]);
+        const float inv = 1.0f / lt;
+        const float lse_val = (mref[qb] + __log2f(lt)) * kLn2;
+        const int qrow = qrow0 + qb * 16, qi = qi0 + qb * 16;
+        if (qi >= a.Sq) continue;
+        if (slot >= 0) {
+            float *orow = pl.ws_o + ((int64_t)slot * BM + qrow) * D;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                f32x4 w;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) w[e] = oacc[db][qb][e] * inv;
+                *reinterpret_cast<f32x4 *>(orow + db * 16 + g * 4) = w;
+            }
+            if (g == 0) pl.ws_lse[(int64_t)slot * BM + qrow] = lse_val;
+        } else {
+            char *orow = static_cast<char *>(a.o) +
+                         ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                const int d = db * 16 + g * 4;
+                if constexpr (OUT_F32) {
+                    f32x4 w;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) w[e] = oacc[db][qb][e] * inv;
+                    *reinterpret_cast<f32x4 *>(orow + d * 4) = w;
+                } else {
+                    bf16x4 w;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) w[e] = (__bf16)(oacc[db][qb][e] * inv);
+                    *reinterpret_cast<bf16x4 *>(orow + d * 2) = w;
+                }
+            }
+            if (a.lse != nullptr && g == 0) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = lse_val;
+        }
+    }
 }
 
 // Log-sum-exp combination of the key-range partials of each split tile
