@@ -30,6 +30,9 @@ def open_library(path: str) -> ctypes.CDLL:
     lib.oracle_merge.restype = i32
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = i32
+    lib.oracle_norm_rope.argtypes = [p, i64, i64, i64, p, p, i32, i32, i32, i32, i32, i32, i32, i32,
+                                     ctypes.c_float, ctypes.c_float]
+    lib.oracle_norm_rope.restype = i32
     return lib
 
 
@@ -82,6 +85,24 @@ def merge(o_parts, lse_parts, lib=None):
     if rc != 0:
         raise ValueError("oracle_merge rejected its arguments")
     return o, lse
+
+
+def norm_rope(x: np.ndarray, w: np.ndarray, grid, token0: int = 0, eps: float = 1e-6, theta: float = 10000.0,
+              lib=None):
+    """q or k RMSNorm over all H*D channels of a token, then 3D rotary
+    embedding per head (see oracle_norm_rope in oracle.c).  x: bf16 bits
+    [B, S, H, D]; w: bf16 bits [H*D]; grid = (frames, rows, cols).  Returns
+    float64 [B, S, H, D]."""
+    B, S, H, D = x.shape
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    assert w.shape == (H * D,)
+    y = np.empty((B, S, H, D), dtype=np.float64)
+    rc = (lib or _load()).oracle_norm_rope(x.ctypes.data, *_strides(x), w.ctypes.data, y.ctypes.data, B, S, H, D,
+                                           int(grid[0]), int(grid[1]), int(grid[2]), int(token0),
+                                           ctypes.c_float(eps), ctypes.c_float(theta))
+    if rc != 0:
+        raise ValueError("oracle_norm_rope rejected its arguments")
+    return y
 
 
 def num_threads() -> int:

@@ -171,3 +171,82 @@ int oracle_num_threads(void)
     }
     return n;
 }
+
+/*
+ * q/k RMSNorm + 3D rotary position embedding: the steps between the QKV
+ * projection and self-attention in a block of the video diffusion
+ * transformer (the backbone of Sec. 3.4; the block shape -- RMSNorm on q and
+ * k, rotary embedding split over frame / row / column -- is the workload's
+ * configuration, the paper does not print it).  Per batch b and token t, with
+ * x the C = H*D values of the token (all heads) and w the C norm weights:
+ *
+ *     r   = 1 / sqrt(sum_c x_c^2 / C + eps)
+ *     y_c = x_c * r * w_c
+ *
+ * then per head, on pairs (y_2i, y_2i+1), i = 0..D/2-1, a rotation by
+ *
+ *     angle_i = pos_a * theta^(-2 k / d_a)
+ *
+ * where pair i belongs to axis a = frame for i < Pf, row for Pf <= i < Pf+Ph,
+ * column otherwise, k is its index within that axis, d_a = 2 * (pairs of the
+ * axis), Ph = Pw = D/6 (integer division) and Pf = D/2 - Ph - Pw (22/21/21
+ * pairs, 44/42/42 dims, at D = 128); the token's global index g = token0 + t
+ * in (frame, row, column) raster order over a grid_f x grid_h x grid_w
+ * latent grid gives pos_frame = g / (grid_h grid_w),
+ * pos_row = (g / grid_w) % grid_h, pos_col = g % grid_w:
+ *
+ *     (y_2i, y_2i+1) -> (y_2i cos a - y_2i+1 sin a,  y_2i sin a + y_2i+1 cos a)
+ *
+ * This is the rotary embedding of RoFormer (rotation of coordinate pairs by
+ * position times a geometric frequency), applied per axis.  eps and theta are
+ * the caller's float32 values widened to double; all arithmetic in double.
+ * x: bf16 [B, S, H, D] with element strides; w: bf16 [H*D]; y: double
+ * [B, S, H, D] contiguous.  Returns 0, or -1 on bad sizes.
+ */
+int oracle_norm_rope(const uint16_t *x, int64_t x_sb, int64_t x_ss, int64_t x_sh, const uint16_t *w,
+                     double *y, int B, int S, int H, int D, int grid_f, int grid_h, int grid_w, int token0,
+                     float eps_f32, float theta_f32)
+{
+    if (B < 0 || S < 0 || H < 1 || D < 6 || D % 2 != 0 || grid_f < 1 || grid_h < 1 || grid_w < 1 ||
+        token0 < 0 || (int64_t)token0 + S > (int64_t)grid_f * grid_h * grid_w)
+        return -1;
+    const double eps = (double)eps_f32, theta = (double)theta_f32;
+    const int C = H * D, P = D / 2;
+    const int ph = D / 6, pw = D / 6, pf = P - ph - pw;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int b = 0; b < B; ++b)
+        for (int t = 0; t < S; ++t) {
+            double ss = 0.0;
+            for (int h = 0; h < H; ++h)
+                for (int d = 0; d < D; ++d) {
+                    const double xv = bf16_to_double(x[b * x_sb + t * x_ss + h * x_sh + d]);
+                    ss += xv * xv;
+                }
+            const double r = 1.0 / sqrt(ss / C + eps);
+            const int64_t g = (int64_t)token0 + t;
+            const double pos[3] = {(double)(g / ((int64_t)grid_h * grid_w)), (double)((g / grid_w) % grid_h),
+                                   (double)(g % grid_w)};
+            for (int h = 0; h < H; ++h) {
+                double *yr = y + (((int64_t)b * S + t) * H + h) * D;
+                for (int d = 0; d < D; ++d)
+                    yr[d] = bf16_to_double(x[b * x_sb + t * x_ss + h * x_sh + d]) * r *
+                            bf16_to_double(w[h * D + d]);
+                for (int i = 0; i < P; ++i) {
+                    int axis, kk, pairs;
+                    if (i < pf) {
+                        axis = 0, kk = i, pairs = pf;
+                    } else if (i < pf + ph) {
+                        axis = 1, kk = i - pf, pairs = ph;
+                    } else {
+                        axis = 2, kk = i - pf - ph, pairs = pw;
+                    }
+                    const double ang = pos[axis] * pow(theta, -2.0 * kk / (2.0 * pairs));
+                    const double c = cos(ang), sn = sin(ang);
+                    const double a0 = yr[2 * i], a1 = yr[2 * i + 1];
+                    yr[2 * i] = a0 * c - a1 * sn;
+                    yr[2 * i + 1] = a0 * sn + a1 * c;
+                }
+            }
+        }
+    return 0;
+}
