@@ -111,14 +111,55 @@ def copy_reference(torch, dev, args):
                       "GB/s": 8 * n / (ms * 1e-3) / 1e9}), flush=True)
 
 
+def normrope_bench(torch, dev, args):
+    """q/k RMSNorm + 3D rotary embedding at the window shape (B=1, 10920
+    tokens = 7 x 30 x 52, 12 heads x 128): HBM-bound, algorithmic bytes =
+    q and k read once and written once (bf16) plus the two weight vectors."""
+    from paper_2607_28144_amd import api, synth
+    W = WINDOW
+    B, S, H, D = W["B"], W["S"], W["H"], W["D"]
+    rng = np.random.default_rng(7)
+
+    def to_dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    q = to_dev(synth.normal_bf16(rng, (B, S, H, D)))
+    k = to_dev(synth.normal_bf16(rng, (B, S, H, D)))
+    wq = to_dev(synth.f32_to_bf16_bits(1.0 + 0.1 * rng.standard_normal(H * D).astype(np.float32)))
+    wk = to_dev(synth.f32_to_bf16_bits(1.0 + 0.1 * rng.standard_normal(H * D).astype(np.float32)))
+    qo, ko = torch.empty_like(q), torch.empty_like(k)
+    grid = (7, 30, 52)
+    for _ in range(args.warmup):
+        api.qk_norm_rope(q, k, wq, wk, grid, q_out=qo, k_out=ko)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        api.qk_norm_rope(q, k, wq, wk, grid, q_out=qo, k_out=ko)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    nbytes = 4 * B * S * H * D * 2 + 2 * H * D * 2
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    print(json.dumps({"metric": "q/k RMSNorm + 3D RoPE HBM throughput at the window shape", "value": gbs,
+                      "unit": "GB/s", "ms": ms, "bytes": nbytes, "steps": args.steps, "warmup": args.warmup,
+                      "config": {"workload": "q/k RMSNorm over 1536 channels + 3D RoPE 44/42/42, B=1 S=10920 "
+                                             "(7x30x52) H=12 d=128 bf16"},
+                      "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                                   "frac": gbs / PEAK_HBM_GBS, "traffic": None}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=20, help="untimed steps (the clock settles under load)")
-    ap.add_argument("--only", choices=["self", "cross", "share", "copy"], default=None,
+    ap.add_argument("--only", choices=["self", "cross", "share", "copy", "normrope"], default=None,
                     help="time one component alone (for profiling); 'copy' runs a plain 1 GiB elementwise "
-                         "copy kernel, the reference for scaling HBM byte counters")
+                         "copy kernel, the reference for scaling HBM byte counters; 'normrope' times the q/k "
+                         "RMSNorm + 3D rotary embedding that produces the window's attention inputs (not part "
+                         "of the attention step)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle sample")
     args = ap.parse_args()
@@ -138,6 +179,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.only == "copy":
         copy_reference(torch, dev, args)
+        return
+    if args.only == "normrope":
+        normrope_bench(torch, dev, args)
         return
 
     def to_dev(bits):

@@ -151,6 +151,43 @@ regenvc_status regenvc_cross_attn_fwd(const regenvc_tensor *q,
                                       int32_t Sctx, int32_t D, float softmax_scale,
                                       void *stream);
 
+/* q/k RMSNorm + 3D rotary position embedding: the steps that turn the QKV
+   projection's q and k into the attention inputs in a block of the video
+   diffusion transformer (the backbone of Sec. 3.4, whose blocks the paper's
+   compilation step fuses pointwise, Sec. 3.8).  Per batch b and token t, x
+   being q (or k) over all H*D channels of the token and w = w_q (or w_k):
+     r   = 1 / sqrt(sum_c x_c^2 / (H*D) + eps)
+     y_c = x_c * r * w_c
+   then in every head, each pair (y_2i, y_2i+1), i < D/2, is rotated by
+     angle = pos_a * theta^(-2k / d_a)
+     (y_2i, y_2i+1) <- (y_2i cos - y_2i+1 sin, y_2i sin + y_2i+1 cos)
+   where the pairs are split over the latent grid's axes a = frame, row,
+   column (Ph = Pw = D/6 pairs for rows and columns, the other D/2 - 2 D/6 for
+   frames: 22/21/21 at D = 128), k is the pair's index within its axis and
+   d_a = 2 * (its axis' pairs).  The token's position comes from its global
+   index g = token0 + t in (frame, row, column) raster order on a
+   grid_f x grid_h x grid_w grid: frame g / (grid_h grid_w), row
+   (g / grid_w) % grid_h, column g % grid_w.
+     q_in, k_in, q_out, k_out: bf16 [B,S,H,D] views (as above); an output may
+       be exactly its own input (same pointer and strides), otherwise no
+       output may overlap any input or the other output.  Outputs are
+       rounded to bf16 (nearest even).
+     w_q, w_k: bf16 [H*D] contiguous, 16-byte aligned.
+     D in {64, 128}; H >= 1; H*D <= 8192; 1 <= grid sizes <= 4096;
+     token0 >= 0; token0 + S <= grid_f*grid_h*grid_w; eps finite >= 0
+     (usual 1e-6); theta finite > 0 (usual 10000).
+   Arithmetic is float32: the angle pos_a * theta^(-2k/d_a) is formed in
+   float32 (relative error ~2^-23, i.e. at most ~5e-4 rad at position 4095)
+   and reduced to one turn before the hardware sine and cosine.  Non-finite
+   inputs give non-finite outputs.  Allocates nothing.  HBM-bound: every q
+   and k element is read once and written once. */
+regenvc_status regenvc_qk_norm_rope(const regenvc_tensor *q_in, const regenvc_tensor *k_in,
+                                    const void *w_q, const void *w_k,
+                                    const regenvc_tensor *q_out, const regenvc_tensor *k_out,
+                                    int32_t B, int32_t S, int32_t H, int32_t D,
+                                    int32_t grid_f, int32_t grid_h, int32_t grid_w, int32_t token0,
+                                    float eps, float theta, void *stream);
+
 /* Work plan of one attention call (regenvc_attn_fwd, regenvc_attn_partial_fwd
    or regenvc_cross_attn_fwd) of the given shape on a device with n_cu
    compute units (the calls themselves use the current device's count, 256

@@ -2,12 +2,14 @@
 
 Exact non-causal softmax attention for one GPU's share of a sequence-parallel
 video diffusion transformer, its per-chunk partials and log-sum-exp merge,
-and cross-attention to conditioning tokens -- hand-written HIP kernels behind
+cross-attention to conditioning tokens, and the q/k RMSNorm + 3D rotary
+embedding that produce the attention inputs -- hand-written HIP kernels behind
 a C ABI (include/regenvc_attn.h).  Import is cheap: the library and torch are
 loaded on first use.
 """
 
-__all__ = ["attn_fwd", "attn_partial_fwd", "lse_merge", "cross_attn_fwd", "attn_plan", "RegenvcError"]
+__all__ = ["attn_fwd", "attn_partial_fwd", "lse_merge", "cross_attn_fwd", "attn_plan", "qk_norm_rope",
+           "RegenvcError"]
 
 
 def __getattr__(name):

@@ -43,6 +43,8 @@ _SIGNATURES = {
     "regenvc_cross_attn_fwd": [_PT, _PT, _PT, _PT, ctypes.c_int, ctypes.c_void_p,
                                _i32, _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_void_p],
     "regenvc_attn_plan_query": [_i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(AttnPlan)],
+    "regenvc_qk_norm_rope": [_PT, _PT, ctypes.c_void_p, ctypes.c_void_p, _PT, _PT, _i32, _i32, _i32, _i32,
+                             _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_float, ctypes.c_void_p],
 }
 
 _lib = None

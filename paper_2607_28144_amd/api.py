@@ -138,3 +138,33 @@ def attn_plan(B: int, H: int, Sq: int, Skv: int, D: int, n_cu: int = 256) -> dic
     st = _lib.load().regenvc_attn_plan_query(B, H, Sq, Skv, D, n_cu, ctypes.byref(plan))
     _lib.check(st, "regenvc_attn_plan_query")
     return {f: getattr(plan, f) for f, _ in _lib.AttnPlan._fields_}
+
+
+def qk_norm_rope(q: torch.Tensor, k: torch.Tensor, w_q: torch.Tensor, w_k: torch.Tensor, grid,
+                 token0: int = 0, eps: float = 1e-6, theta: float = 10000.0,
+                 q_out: Optional[torch.Tensor] = None, k_out: Optional[torch.Tensor] = None
+                 ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """q/k RMSNorm over all H*D channels of each token, then 3D rotary
+    embedding per head over a (frames, rows, cols) latent grid
+    (regenvc_qk_norm_rope).  q, k: bf16 [B, S, H, D]; w_q, w_k: bf16 [H*D]
+    contiguous.  Outputs may be q and k themselves (in place).  Returns
+    (q_out, k_out)."""
+    B, S, H, D = q.shape
+    if tuple(k.shape) != (B, S, H, D):
+        raise ValueError(f"k shape {tuple(k.shape)} does not match q {tuple(q.shape)}")
+    for name, w in (("w_q", w_q), ("w_k", w_k)):
+        if not isinstance(w, torch.Tensor) or w.dtype != torch.bfloat16 or w.device != q.device \
+                or not w.is_contiguous() or w.numel() != H * D:
+            raise ValueError(f"{name} must be a contiguous bf16 device tensor of {H * D} elements")
+    q_out = torch.empty_like(q) if q_out is None else q_out
+    k_out = torch.empty_like(k) if k_out is None else k_out
+    qi, ki = _desc(q, "q", torch.bfloat16), _desc(k, "k", torch.bfloat16)
+    qo, ko = _desc(q_out, "q_out", torch.bfloat16), _desc(k_out, "k_out", torch.bfloat16)
+    gf, gh, gw = (int(x) for x in grid)
+    lib = _lib.load()
+    with torch.cuda.device(q.device):
+        st = lib.regenvc_qk_norm_rope(ctypes.byref(qi), ctypes.byref(ki), w_q.data_ptr(), w_k.data_ptr(),
+                                      ctypes.byref(qo), ctypes.byref(ko), B, S, H, D, gf, gh, gw, int(token0),
+                                      float(eps), float(theta), _stream(q.device))
+    _lib.check(st, "regenvc_qk_norm_rope")
+    return q_out, k_out

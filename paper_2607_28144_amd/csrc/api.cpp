@@ -324,6 +324,74 @@ regenvc_status regenvc_lse_merge(const float *const *o_parts, const float *const
     return launched(regenvc::launch_merge(m, static_cast<hipStream_t>(stream)), "regenvc_lse_merge");
 }
 
+regenvc_status regenvc_qk_norm_rope(const regenvc_tensor *q_in, const regenvc_tensor *k_in, const void *w_q,
+                                    const void *w_k, const regenvc_tensor *q_out, const regenvc_tensor *k_out,
+                                    int32_t B, int32_t S, int32_t H, int32_t D, int32_t grid_f, int32_t grid_h,
+                                    int32_t grid_w, int32_t token0, float eps, float theta, void *stream)
+{
+    const char *fn = "regenvc_qk_norm_rope";
+    if (B < 0 || S < 0 || H < 1)
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: bad size (B=%d S=%d H=%d)", fn, B, S, H);
+    if (D != 64 && D != 128) return fail(REGENVC_ERR_UNSUPPORTED, "%s: head dim D=%d (only 64 and 128)", fn, D);
+    if ((int64_t)H * D > 8192)
+        return fail(REGENVC_ERR_UNSUPPORTED, "%s: H*D=%lld channels per token (at most 8192)", fn,
+                    (long long)H * D);
+    if (grid_f < 1 || grid_h < 1 || grid_w < 1 || token0 < 0)
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: bad grid %d x %d x %d or token0=%d", fn, grid_f, grid_h, grid_w,
+                    token0);
+    if (grid_f > 4096 || grid_h > 4096 || grid_w > 4096)
+        return fail(REGENVC_ERR_UNSUPPORTED, "%s: grid %d x %d x %d has an axis longer than 4096", fn, grid_f, grid_h,
+                    grid_w);
+    if ((int64_t)token0 + S > (int64_t)grid_f * grid_h * grid_w)
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: tokens %d..%lld lie outside the %d x %d x %d grid", fn, token0,
+                    (long long)token0 + S - 1, grid_f, grid_h, grid_w);
+    if (!std::isfinite(eps) || eps < 0.f) return fail(REGENVC_ERR_INVALID_ARG, "%s: eps must be finite and >= 0", fn);
+    if (!std::isfinite(theta) || !(theta > 0.f))
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: theta must be finite and > 0", fn);
+    if (!q_in || !k_in || !q_out || !k_out) return fail(REGENVC_ERR_INVALID_ARG, "%s: descriptor is NULL", fn);
+    if (w_q == nullptr || w_k == nullptr) return fail(REGENVC_ERR_INVALID_ARG, "%s: weight pointer is NULL", fn);
+    if (reinterpret_cast<uintptr_t>(w_q) % 16 != 0 || reinterpret_cast<uintptr_t>(w_k) % 16 != 0)
+        return fail(REGENVC_ERR_UNSUPPORTED, "%s: weight pointer is not 16-byte aligned", fn);
+    if (B == 0 || S == 0) {
+        g_last_error[0] = '\0';
+        return REGENVC_OK;
+    }
+    regenvc_status st;
+    Extent eqi, eki, eqo, eko;
+    if ((st = check_view("q_in", q_in, B, S, H, D, 2, &eqi)) != REGENVC_OK) return st;
+    if ((st = check_view("k_in", k_in, B, S, H, D, 2, &eki)) != REGENVC_OK) return st;
+    if ((st = check_view("q_out", q_out, B, S, H, D, 2, &eqo)) != REGENVC_OK) return st;
+    if ((st = check_view("k_out", k_out, B, S, H, D, 2, &eko)) != REGENVC_OK) return st;
+    if (!view_is_injective(q_out, B, S, H, D) || !view_is_injective(k_out, B, S, H, D))
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: an output has overlapping rows (strides)", fn);
+    auto same_view = [](const regenvc_tensor *a, const regenvc_tensor *b) {
+        return a->ptr == b->ptr && a->stride_b == b->stride_b && a->stride_s == b->stride_s &&
+               a->stride_h == b->stride_h;
+    };
+    const Extent ewq = flat_extent(w_q, (int64_t)H * D, 2), ewk = flat_extent(w_k, (int64_t)H * D, 2);
+    if (overlap(eqo, eko)) return fail(REGENVC_ERR_INVALID_ARG, "%s: q_out overlaps k_out", fn);
+    if ((overlap(eqo, eqi) && !same_view(q_out, q_in)) || overlap(eqo, eki) || overlap(eqo, ewq) ||
+        overlap(eqo, ewk))
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: q_out overlaps an input (other than being q_in itself)", fn);
+    if ((overlap(eko, eki) && !same_view(k_out, k_in)) || overlap(eko, eqi) || overlap(eko, ewq) ||
+        overlap(eko, ewk))
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: k_out overlaps an input (other than being k_in itself)", fn);
+    if ((st = check_device()) != REGENVC_OK) return st;
+
+    regenvc::NormRopeArgs a{};
+    a.q_in = q_in->ptr, a.k_in = k_in->ptr, a.w_q = w_q, a.w_k = w_k;
+    a.q_out = q_out->ptr, a.k_out = k_out->ptr;
+    a.qi_sb = q_in->stride_b, a.qi_ss = q_in->stride_s, a.qi_sh = q_in->stride_h;
+    a.ki_sb = k_in->stride_b, a.ki_ss = k_in->stride_s, a.ki_sh = k_in->stride_h;
+    a.qo_sb = q_out->stride_b, a.qo_ss = q_out->stride_s, a.qo_sh = q_out->stride_h;
+    a.ko_sb = k_out->stride_b, a.ko_ss = k_out->stride_s, a.ko_sh = k_out->stride_h;
+    a.B = B, a.S = S, a.H = H, a.D = D;
+    a.grid_f = grid_f, a.grid_h = grid_h, a.grid_w = grid_w, a.token0 = token0;
+    a.eps = eps;
+    a.log2_theta = std::log2(theta);
+    return launched(regenvc::launch_norm_rope(a, static_cast<hipStream_t>(stream)), fn);
+}
+
 regenvc_status regenvc_attn_plan_query(int32_t B, int32_t H, int32_t Sq, int32_t Skv, int32_t D, int32_t n_cu,
                                        regenvc_attn_plan *plan)
 {

@@ -60,6 +60,21 @@ struct FillArgs {  // empty-chunk partial: O = 0, LSE = -inf
     int32_t B, H, Sq, D;
 };
 
+// q/k RMSNorm over all H*D channels of a token + 3D rotary embedding per
+// head; q/k in and out bf16 [B,S,H,D] (element strides, d contiguous; an
+// output may be its own input); w_q/w_k bf16 [H*D].
+struct NormRopeArgs {
+    const void *q_in, *k_in, *w_q, *w_k;
+    void *q_out, *k_out;
+    int64_t qi_sb, qi_ss, qi_sh;
+    int64_t ki_sb, ki_ss, ki_sh;
+    int64_t qo_sb, qo_ss, qo_sh;
+    int64_t ko_sb, ko_ss, ko_sh;
+    int32_t B, S, H, D;
+    int32_t grid_f, grid_h, grid_w, token0;
+    float eps, log2_theta;
+};
+
 // Work plan of an attention launch of this shape on n_cu compute units
 // (host-only); false if the shape has no valid plan (Skv < 1, too many tiles).
 bool plan_attn(int B, int H, int Sq, int Skv, int D, int n_cu, AttnPlan *out);
@@ -69,5 +84,6 @@ size_t workspace_bytes(const AttnPlan &pl, int D);
 hipError_t launch_attn(const AttnArgs &a, hipStream_t stream);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t stream);
 hipError_t launch_empty_partial(const FillArgs &a, hipStream_t stream);
+hipError_t launch_norm_rope(const NormRopeArgs &a, hipStream_t stream);
 
 }  // namespace regenvc

@@ -134,3 +134,44 @@ def test_merge_validation(lib):
 def test_valid_arguments_without_a_gpu_report_a_hip_error(lib):
     # Validation passes, then the device query fails: nothing can be launched.
     expect(lib, attn(lib), _lib.ERR_HIP, "hip")
+
+
+def norm_rope(lib, q=None, k=None, qo=None, ko=None, wq=FAKE + 0x6000000, wk=FAKE + 0x6100000, B=1, S=64, H=2,
+              D=128, grid=(4, 4, 4), token0=0, eps=1e-6, theta=10000.0):
+    q = q if q is not None else T(FAKE, S=S, H=H, D=D)
+    k = k if k is not None else T(FAKE + 0x1000000, S=S, H=H, D=D)
+    qo = qo if qo is not None else T(FAKE + 0x2000000, S=S, H=H, D=D)
+    ko = ko if ko is not None else T(FAKE + 0x3000000, S=S, H=H, D=D)
+    byref = lambda t: ctypes.byref(t) if t is not False else None  # noqa: E731
+    return lib.regenvc_qk_norm_rope(byref(q), byref(k), wq, wk, byref(qo), byref(ko), B, S, H, D, *grid, token0,
+                                    eps, theta, None)
+
+
+def test_norm_rope_validation(lib):
+    expect(lib, norm_rope(lib, D=96), _lib.ERR_UNSUPPORTED, "head dim")
+    expect(lib, norm_rope(lib, H=0), _lib.ERR_INVALID_ARG, "bad size")
+    expect(lib, norm_rope(lib, H=65, D=128), _lib.ERR_UNSUPPORTED, "channels")
+    expect(lib, norm_rope(lib, grid=(4, 4, 3)), _lib.ERR_INVALID_ARG, "outside")
+    expect(lib, norm_rope(lib, token0=1), _lib.ERR_INVALID_ARG, "outside")
+    expect(lib, norm_rope(lib, grid=(0, 4, 4)), _lib.ERR_INVALID_ARG, "grid")
+    expect(lib, norm_rope(lib, grid=(1, 1, 4097)), _lib.ERR_UNSUPPORTED, "longer than 4096")
+    expect(lib, norm_rope(lib, eps=-1.0), _lib.ERR_INVALID_ARG, "eps")
+    expect(lib, norm_rope(lib, eps=float("nan")), _lib.ERR_INVALID_ARG, "eps")
+    expect(lib, norm_rope(lib, theta=0.0), _lib.ERR_INVALID_ARG, "theta")
+    expect(lib, norm_rope(lib, wq=0), _lib.ERR_INVALID_ARG, "weight")
+    expect(lib, norm_rope(lib, wk=FAKE + 8), _lib.ERR_UNSUPPORTED, "aligned")
+    expect(lib, norm_rope(lib, q=False), _lib.ERR_INVALID_ARG, "NULL")
+    expect(lib, norm_rope(lib, qo=T(FAKE + 0x1000000)), _lib.ERR_INVALID_ARG, "q_out overlaps")
+    expect(lib, norm_rope(lib, qo=T(FAKE + 0x3000000)), _lib.ERR_INVALID_ARG, "q_out overlaps k_out")
+    expect(lib, norm_rope(lib, ko=T(FAKE + 0x6000000)), _lib.ERR_INVALID_ARG, "k_out overlaps")
+    expect(lib, norm_rope(lib, qo=T(FAKE + 0x2000000, ss=0)), _lib.ERR_INVALID_ARG, "overlapping rows")
+    expect(lib, norm_rope(lib, qo=T(FAKE + 0x10, S=64)), _lib.ERR_INVALID_ARG, "q_out overlaps")  # partial alias
+    expect(lib, norm_rope(lib, B=0), _lib.OK)
+    expect(lib, norm_rope(lib, S=0), _lib.OK)
+
+
+@pytest.mark.skipif(has_gpu_node(), reason="would reach a launch on fake addresses on a GPU machine")
+def test_norm_rope_in_place_passes_validation(lib):
+    # exact aliasing of an output with its own input is allowed: validation
+    # passes and the device query is what fails here
+    expect(lib, norm_rope(lib, qo=T(FAKE), ko=T(FAKE + 0x1000000)), _lib.ERR_HIP, "hip")
