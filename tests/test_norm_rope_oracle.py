@@ -180,10 +180,13 @@ def test_planted_mistakes_are_caught(name, old, new):
     assert src.count(old) == 1, f"mutation site for '{name}' not found exactly once"
     tmp = tempfile.mkdtemp(prefix="norm_rope_mutant_")
     try:
-        path = os.path.join(tmp, "m.c")
+        # a file name no other loaded library has: the dynamic loader may hand
+        # back an already loaded object for a path or file it has seen before
+        tag = "".join(ch if ch.isalnum() else "_" for ch in name)
+        path = os.path.join(tmp, f"norm_rope_mutant_{tag}.c")
         with open(path, "w") as f:
             f.write(src.replace(old, new))
-        lib = oracle.open_library(oracle_build.build(source=path, out=os.path.join(tmp, "m.so")))
+        lib = oracle.open_library(oracle_build.build(source=path, out=path[:-2] + ".so"))
         assert not _pins_hold(lib), f"planted mistake '{name}' was not caught by the pins"
     finally:
         shutil.rmtree(tmp, ignore_errors=True)

@@ -312,10 +312,12 @@ def test_planted_mistakes_are_caught():
     try:
         for i, (name, old, new) in enumerate(MUTANTS):
             assert src.count(old) == 1, f"mutation site for '{name}' not found exactly once"
-            path = os.path.join(tmp, f"m{i}.c")
+            # a file name no other loaded library has (the dynamic loader may
+            # hand back an already loaded object it matches by name)
+            path = os.path.join(tmp, f"attn_mutant_{i}.c")
             with open(path, "w") as f:
                 f.write(src.replace(old, new))
-            so = oracle_build.build(source=path, out=os.path.join(tmp, f"m{i}.so"))
+            so = oracle_build.build(source=path, out=os.path.join(tmp, f"attn_mutant_{i}.so"))
             lib = oracle.open_library(so)
             assert not _pins_hold(lib), f"planted mistake '{name}' was not caught by the pins"
     finally:
