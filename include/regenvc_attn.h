@@ -8,7 +8,8 @@
  *   - Ring streams key/value blocks between GPUs and combines them
  *     online-softmax style: one partial result per key/value chunk, then a
  *     log-sum-exp merge that is exact up to reduction order
- *                            -> regenvc_attn_partial_fwd + regenvc_lse_merge
+ *                            -> regenvc_attn_partial_fwd + regenvc_lse_merge,
+ *                               or regenvc_attn_ring_accumulate (merge fused)
  *   - the conditioning path (Sec. 3.9, "Hybrid CPU-GPU deployment") streams
  *     precomputed text/image key/value tensors to the GPU, which the video
  *     tokens cross-attend to                         -> regenvc_cross_attn_fwd
@@ -139,6 +140,35 @@ regenvc_status regenvc_lse_merge(const float *const *o_parts,
                                  const regenvc_tensor *o, regenvc_dtype o_dtype,
                                  float *lse, int32_t B, int32_t H, int32_t Sq,
                                  int32_t D, void *stream);
+
+/* Ring accumulate (Sec. 3.5: Ring combines the streamed key/value blocks
+   online-softmax style): partial attention over ONE key/value chunk whose
+   epilogue merges the result straight into the running state of the chunks
+   already processed, so no separate merge pass and no per-chunk partial
+   buffers are needed.  Per row, with (O_run, L_run) the running state and
+   (O_c, L_c) the chunk's normalized result and LSE:
+     L = log(exp L_run + exp L_c);  O = exp(L_run - L) O_run + exp(L_c - L) O_c
+   (the regenvc_lse_merge identity for two parts).
+     o_run: f32 [B,Sq,H,D], the normalized output over the chunks so far;
+       read only where lse_run is finite (a row with lse_run = -inf has seen
+       no key and its o_run may hold anything)
+     lse_run: f32 [B,H,Sq], required; read, then overwritten in place with L
+     o_out: NULL writes O back into o_run (f32, o_dtype must be
+       REGENVC_F32); otherwise O goes to o_out in o_dtype (bf16 or f32, e.g.
+       the final chunk's bf16 output) and o_run is only read.  o_out may be
+       o_run itself (same pointer and strides, f32) but must not otherwise
+       overlap it.
+     k_chunk/v_chunk: the chunk as a plain view, as in regenvc_attn_partial_fwd
+   Skv_chunk must be >= 1.  A ring starts from regenvc_attn_partial_fwd on its
+   first chunk, or from lse_run filled with -inf. */
+regenvc_status regenvc_attn_ring_accumulate(const regenvc_tensor *q,
+                                            const regenvc_tensor *k_chunk,
+                                            const regenvc_tensor *v_chunk,
+                                            const regenvc_tensor *o_run, float *lse_run,
+                                            const regenvc_tensor *o_out, regenvc_dtype o_dtype,
+                                            int32_t B, int32_t H, int32_t Sq,
+                                            int32_t Skv_chunk, int32_t D,
+                                            float softmax_scale, void *stream);
 
 /* Cross-attention of the video tokens to Sctx conditioning tokens whose
    key/value tensors were precomputed off-GPU and uploaded (Sec. 3.9).

@@ -87,6 +87,20 @@ def merge(o_parts, lse_parts, lib=None):
     return o, lse
 
 
+def ring_accumulate(o_run, lse_run, q, k, v, scale: float, lib=None):
+    """One ring step (paper Sec. 3.5, key/value blocks combined online-softmax
+    style): the attention of q over this key/value chunk, merged into the
+    running state (o_run, lse_run) of the chunks seen so far by the same
+    log-sum-exp identity as merge().  Rows whose lse_run is -inf have seen no
+    key; their o_run is not used.  Returns the new (O, LSE), float64."""
+    o_c, l_c = attn(q, k, v, scale, lib)
+    lse_run = np.asarray(lse_run, dtype=np.float64)
+    fresh = np.isneginf(lse_run)                        # [B, H, Sq]
+    o_run = np.array(o_run, dtype=np.float64)
+    o_run[np.transpose(fresh, (0, 2, 1))] = 0.0         # [B, Sq, H] rows
+    return merge([o_run, o_c], [lse_run, l_c], lib)
+
+
 def norm_rope(x: np.ndarray, w: np.ndarray, grid, token0: int = 0, eps: float = 1e-6, theta: float = 10000.0,
               lib=None):
     """q or k RMSNorm over all H*D channels of a token, then 3D rotary

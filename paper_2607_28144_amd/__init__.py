@@ -3,12 +3,13 @@
 Exact non-causal softmax attention for one GPU's share of a sequence-parallel
 video diffusion transformer, its per-chunk partials and log-sum-exp merge,
 cross-attention to conditioning tokens, and the q/k RMSNorm + 3D rotary
-embedding that produce the attention inputs -- hand-written HIP kernels behind
+embedding that produce the attention inputs (plus a ring step that merges a
+chunk's result straight into the running output) -- hand-written HIP kernels behind
 a C ABI (include/regenvc_attn.h).  Import is cheap: the library and torch are
 loaded on first use.
 """
 
-__all__ = ["attn_fwd", "attn_partial_fwd", "lse_merge", "cross_attn_fwd", "attn_plan", "qk_norm_rope",
+__all__ = ["attn_fwd", "attn_partial_fwd", "lse_merge", "attn_ring_accumulate", "cross_attn_fwd", "attn_plan", "qk_norm_rope",
            "RegenvcError"]
 
 

@@ -89,6 +89,41 @@ def attn_partial_fwd(q: torch.Tensor, k_chunk: torch.Tensor, v_chunk: torch.Tens
     return _attn("regenvc_attn_partial_fwd", q, k_chunk, v_chunk, scale, torch.float32, out, True, lse_out)
 
 
+def attn_ring_accumulate(q: torch.Tensor, k_chunk: torch.Tensor, v_chunk: torch.Tensor, o_run: torch.Tensor,
+                         lse_run: torch.Tensor, scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
+                         out_dtype: torch.dtype = torch.float32) -> torch.Tensor:
+    """Partial attention over one key/value chunk merged into the running
+    state (regenvc_attn_ring_accumulate).  o_run: float32 [B, Sq, H, D]
+    normalized output so far (not read where lse_run is -inf); lse_run:
+    float32 [B, H, Sq], updated in place.  With out=None the merged output
+    goes back into o_run; otherwise into `out` (out_dtype).  Returns the
+    tensor that holds the merged output."""
+    B, Sq, H, D = q.shape
+    Skv = k_chunk.shape[1]
+    if tuple(k_chunk.shape) != (B, Skv, H, D) or tuple(v_chunk.shape) != (B, Skv, H, D):
+        raise ValueError(f"k/v shapes {tuple(k_chunk.shape)}, {tuple(v_chunk.shape)} do not match q {tuple(q.shape)}")
+    if tuple(o_run.shape) != (B, Sq, H, D):
+        raise ValueError(f"o_run shape {tuple(o_run.shape)} does not match q {tuple(q.shape)}")
+    qd, kd = _desc(q, "q", torch.bfloat16), _desc(k_chunk, "k_chunk", torch.bfloat16)
+    vd, rd = _desc(v_chunk, "v_chunk", torch.bfloat16), _desc(o_run, "o_run", torch.float32)
+    lp = _fptr(lse_run, "lse_run", (B, H, Sq))
+    if lp is None:
+        raise ValueError("lse_run is required")
+    if out is None:
+        od, dt, res = None, _lib.F32, o_run
+    else:
+        if tuple(out.shape) != (B, Sq, H, D):
+            raise ValueError(f"out shape {tuple(out.shape)} does not match q {tuple(q.shape)}")
+        od, dt, res = _desc(out, "out", out_dtype), _DT[out_dtype], out
+    lib = _lib.load()
+    with torch.cuda.device(q.device):
+        st = lib.regenvc_attn_ring_accumulate(ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), ctypes.byref(rd),
+                                              lp, ctypes.byref(od) if od is not None else None, dt, B, H, Sq, Skv, D,
+                                              _scale(scale, D), _stream(q.device))
+    _lib.check(st, "regenvc_attn_ring_accumulate")
+    return res
+
+
 def cross_attn_fwd(q: torch.Tensor, k_ctx: torch.Tensor, v_ctx: torch.Tensor, scale: Optional[float] = None,
                    out_dtype: torch.dtype = torch.bfloat16, out: Optional[torch.Tensor] = None,
                    return_lse: bool = True, lse_out: Optional[torch.Tensor] = None

@@ -151,10 +151,17 @@ regenvc_status launched(hipError_t e, const char *what)
     return REGENVC_OK;
 }
 
+bool same_view(const regenvc_tensor *a, const regenvc_tensor *b)
+{
+    return a->ptr == b->ptr && a->stride_b == b->stride_b && a->stride_s == b->stride_s && a->stride_h == b->stride_h;
+}
+
+// run_o (ring accumulate only): f32 running output, read; lse is then the
+// running LSE, read and rewritten in place; o may be run_o itself (f32).
 regenvc_status attn_common(const char *fn, const regenvc_tensor *q, const regenvc_tensor *k,
                            const regenvc_tensor *v, const regenvc_tensor *o, regenvc_dtype o_dtype, float *lse,
                            bool lse_required, int32_t B, int32_t H, int32_t Sq, int32_t Skv, int32_t D, float scale,
-                           void *stream, bool allow_empty_keys)
+                           void *stream, bool allow_empty_keys, const regenvc_tensor *run_o = nullptr)
 {
     regenvc_status st = check_sizes(B, H, Sq, D);
     if (st != REGENVC_OK) return st;
@@ -192,6 +199,18 @@ regenvc_status attn_common(const char *fn, const regenvc_tensor *q, const regenv
         if (overlap(el, eq) || overlap(el, eo) || (Skv > 0 && (overlap(el, ek) || overlap(el, ev))))
             return fail(REGENVC_ERR_INVALID_ARG, "%s: lse overlaps another tensor", fn);
     }
+    if (run_o != nullptr) {
+        Extent er;
+        if ((st = check_view("o_run", run_o, B, Sq, H, D, 4, &er)) != REGENVC_OK) return st;
+        if (!view_is_injective(run_o, B, Sq, H, D))
+            return fail(REGENVC_ERR_INVALID_ARG, "%s: o_run has overlapping rows (strides)", fn);
+        if (overlap(er, eq) || overlap(er, ek) || overlap(er, ev))
+            return fail(REGENVC_ERR_INVALID_ARG, "%s: o_run overlaps an input", fn);
+        if (overlap(er, flat_extent(lse, (int64_t)B * H * Sq, 4)))
+            return fail(REGENVC_ERR_INVALID_ARG, "%s: o_run overlaps lse_run", fn);
+        if (overlap(er, eo) && !(same_view(run_o, o) && o_dtype == REGENVC_F32))
+            return fail(REGENVC_ERR_INVALID_ARG, "%s: o_out overlaps o_run (other than being o_run itself)", fn);
+    }
     if ((st = check_device()) != REGENVC_OK) return st;
 
     if (Skv == 0) {  // empty chunk: the merge identity
@@ -225,6 +244,11 @@ regenvc_status attn_common(const char *fn, const regenvc_tensor *q, const regenv
     a.o_f32 = o_dtype == REGENVC_F32;
     a.scale = scale;
     a.kv_off32 = k->stride_s >= 0 && v->stride_s >= 0 && k->stride_s < (1 << 24) && v->stride_s < (1 << 24);
+    if (run_o != nullptr) {
+        a.run_o = static_cast<const float *>(run_o->ptr);
+        a.run_lse = lse;
+        a.r_sb = run_o->stride_b, a.r_ss = run_o->stride_s, a.r_sh = run_o->stride_h;
+    }
     return launched(regenvc::launch_attn(a, static_cast<hipStream_t>(stream)), fn);
 }
 
@@ -247,6 +271,21 @@ regenvc_status regenvc_attn_partial_fwd(const regenvc_tensor *q, const regenvc_t
 {
     return attn_common("regenvc_attn_partial_fwd", q, k_chunk, v_chunk, o_part, REGENVC_F32, lse_part, true, B, H, Sq,
                        Skv_chunk, D, softmax_scale, stream, true);
+}
+
+regenvc_status regenvc_attn_ring_accumulate(const regenvc_tensor *q, const regenvc_tensor *k_chunk,
+                                            const regenvc_tensor *v_chunk, const regenvc_tensor *o_run,
+                                            float *lse_run, const regenvc_tensor *o_out, regenvc_dtype o_dtype,
+                                            int32_t B, int32_t H, int32_t Sq, int32_t Skv_chunk, int32_t D,
+                                            float softmax_scale, void *stream)
+{
+    const char *fn = "regenvc_attn_ring_accumulate";
+    if (o_run == nullptr) return fail(REGENVC_ERR_INVALID_ARG, "%s: o_run descriptor is NULL", fn);
+    if (o_out == nullptr && o_dtype != REGENVC_F32)
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: the running output o_run is f32 (o_dtype must be F32 without o_out)",
+                    fn);
+    return attn_common(fn, q, k_chunk, v_chunk, o_out ? o_out : o_run, o_dtype, lse_run, true, B, H, Sq, Skv_chunk,
+                       D, softmax_scale, stream, false, o_run);
 }
 
 regenvc_status regenvc_cross_attn_fwd(const regenvc_tensor *q, const regenvc_tensor *k_ctx,
@@ -364,10 +403,6 @@ regenvc_status regenvc_qk_norm_rope(const regenvc_tensor *q_in, const regenvc_te
     if ((st = check_view("k_out", k_out, B, S, H, D, 2, &eko)) != REGENVC_OK) return st;
     if (!view_is_injective(q_out, B, S, H, D) || !view_is_injective(k_out, B, S, H, D))
         return fail(REGENVC_ERR_INVALID_ARG, "%s: an output has overlapping rows (strides)", fn);
-    auto same_view = [](const regenvc_tensor *a, const regenvc_tensor *b) {
-        return a->ptr == b->ptr && a->stride_b == b->stride_b && a->stride_s == b->stride_s &&
-               a->stride_h == b->stride_h;
-    };
     const Extent ewq = flat_extent(w_q, (int64_t)H * D, 2), ewk = flat_extent(w_k, (int64_t)H * D, 2);
     if (overlap(eqo, eko)) return fail(REGENVC_ERR_INVALID_ARG, "%s: q_out overlaps k_out", fn);
     if ((overlap(eqo, eqi) && !same_view(q_out, q_in)) || overlap(eqo, eki) || overlap(eqo, ewq) ||

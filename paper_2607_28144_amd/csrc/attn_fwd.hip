@@ -290,11 +290,72 @@ __device__ __forceinline__ WorkItem work_item(const AttnPlan &pl, int item)
     return w;
 }
 
+// Ring accumulate: how a row's running state (normalized O_run over the key
+// chunks seen so far, and its LSE L_run) and this launch's normalized result
+// (O_c, L_c) combine, by the log-sum-exp identity of the chunk merge:
+// L = log(e^L_run + e^L_c), O = e^(L_run - L) O_run + e^(L_c - L) O_c.  A row
+// with L_run = -inf has seen no key: O_run is not read (it may hold anything).
+struct RunMerge {
+    float wr, wc, lse;
+    bool run;  // O_run enters the result
+};
+__device__ __forceinline__ RunMerge run_merge(float lr, float lc)
+{
+    RunMerge m;
+    m.run = !(lr == -INFINITY);
+    if (!m.run) {
+        m.wr = 0.f;
+        m.wc = 1.f;
+        m.lse = lc;
+        return m;
+    }
+    const float mx = fmaxf(lr, lc);
+    const float er = expf(lr - mx), ec = expf(lc - mx);
+    const float s = er + ec;
+    m.wr = er / s;
+    m.wc = ec / s;
+    m.lse = mx + logf(s);
+    return m;
+}
+
+// Output row of query qi of (b, h) and, in the ring-accumulate mode, the
+// merge weights of that row (w.wc multiplies this launch's normalized O).
+template <bool ACC>
+__device__ __forceinline__ RunMerge out_row_weights(const AttnArgs &a, int b, int h, int qi, float lse_c)
+{
+    if (!ACC || a.run_lse == nullptr) return RunMerge{0.f, 1.f, lse_c, false};
+    return run_merge(a.run_lse[((int64_t)b * a.H + h) * a.Sq + qi], lse_c);
+}
+
+// Four consecutive output values of a row: w.wc * oc (+ w.wr * O_run when the
+// running state enters), stored as f32 or bf16 at element d of the row.
+template <bool OUT_F32>
+__device__ __forceinline__ void put_out4(const AttnArgs &a, char *orow, const float *rrow, const RunMerge &w, int d,
+                                         f32x4 oc)
+{
+    f32x4 r = oc * w.wc;
+    if (w.run) r += *reinterpret_cast<const f32x4 *>(rrow + d) * w.wr;
+    if constexpr (OUT_F32) {
+        *reinterpret_cast<f32x4 *>(orow + d * 4) = r;
+    } else {
+        bf16x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = (__bf16)r[e];
+        *reinterpret_cast<bf16x4 *>(orow + d * 2) = o;
+    }
+}
+
+template <bool ACC>
+__device__ __forceinline__ const float *run_row(const AttnArgs &a, int b, int h, int qi)
+{
+    return !ACC || a.run_o == nullptr ? nullptr : a.run_o + ((int64_t)b * a.r_sb + (int64_t)qi * a.r_ss + (int64_t)h * a.r_sh);
+}
+
 // Epilogue of one lane's query row: O = O^T / l and LSE = ln2 * (m_ref +
 // log2 l), with l the fp32 sum of the weights; a split tile's key range
 // writes its normalized partial to the workspace instead.  lsum is this
 // lane's half of l (the other half is in lane^32).
-template <int D, bool OUT_F32>
+template <int D, bool OUT_F32, bool ACC>
 __device__ __forceinline__ void store_row(const AttnArgs &a, const AttnPlan &pl, const f32x16 (&oacc)[D / 32],
                                           float lsum, float mref, int b, int h, int qi, int qrow, int slot)
 {
@@ -320,24 +381,19 @@ __device__ __forceinline__ void store_row(const AttnArgs &a, const AttnPlan &pl,
     } else {
         char *orow = static_cast<char *>(a.o) +
                      ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
+        RunMerge w = out_row_weights<ACC>(a, b, h, qi, lse_val);
+        w.wc *= inv;
+        const float *rrow = run_row<ACC>(a, b, h, qi);
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
             for (int gq = 0; gq < 4; ++gq) {
-                const int d = db * 32 + gq * 8 + hi * 4;
-                if constexpr (OUT_F32) {
-                    f32x4 w;
+                f32x4 oc;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) w[e] = oacc[db][gq * 4 + e] * inv;
-                    *reinterpret_cast<f32x4 *>(orow + d * 4) = w;
-                } else {
-                    bf16x4 w;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) w[e] = (__bf16)(oacc[db][gq * 4 + e] * inv);
-                    *reinterpret_cast<bf16x4 *>(orow + d * 2) = w;
-                }
+                for (int e = 0; e < 4; ++e) oc[e] = oacc[db][gq * 4 + e];
+                put_out4<OUT_F32>(a, orow, rrow, w, db * 32 + gq * 8 + hi * 4, oc);
             }
-        if (a.lse != nullptr && hi == 0) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = lse_val;
+        if (a.lse != nullptr && hi == 0) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = w.lse;
     }
 }
 
@@ -347,7 +403,9 @@ __device__ __forceinline__ void wait_vmcnt()
     __asm__ volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
 }
 
-template <int D, bool OUT_F32>
+// ACC: the ring-accumulate epilogue (a separate instantiation, so that the
+// plain kernels keep their register allocation).
+template <int D, bool OUT_F32, bool ACC>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 {
@@ -708,7 +766,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         step(t, scur, snext, F_{}, F_{});
     wait_vmcnt<0>();  // the clamped trailing copies must land before the workgroup exits
 
-    store_row<D, OUT_F32>(a, pl, oacc, lsum, mref, b, h, qi, qrow, slot);
+    store_row<D, OUT_F32, ACC>(a, pl, oacc, lsum, mref, b, h, qi, qrow, slot);
 }
 
 // Ping-pong schedule of the same computation (launches with many key tiles).
@@ -741,7 +799,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 // Weights use the speculative reference of the interleaved kernel, checked
 // once per tile (a lane's 16 weights of one query summing to more than
 // kSpecLimit), and the same running sum.
-template <int D, bool OUT_F32>
+template <int D, bool OUT_F32, bool ACC>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
 {
@@ -1118,22 +1176,12 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
         } else {
             char *orow = static_cast<char *>(a.o) +
                          ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
+            RunMerge w = out_row_weights<ACC>(a, b, h, qi, lse_val);
+            w.wc *= inv;
+            const float *rrow = run_row<ACC>(a, b, h, qi);
 #pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                const int d = db * 16 + g * 4;
-                if constexpr (OUT_F32) {
-                    f32x4 w;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) w[e] = oacc[db][qb][e] * inv;
-                    *reinterpret_cast<f32x4 *>(orow + d * 4) = w;
-                } else {
-                    bf16x4 w;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) w[e] = (__bf16)(oacc[db][qb][e] * inv);
-                    *reinterpret_cast<bf16x4 *>(orow + d * 2) = w;
-                }
-            }
-            if (a.lse != nullptr && g == 0) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = lse_val;
+            for (int db = 0; db < DB; ++db) put_out4<OUT_F32>(a, orow, rrow, w, db * 16 + g * 4, oacc[db][qb]);
+            if (a.lse != nullptr && g == 0) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = w.lse;
         }
     }
 }
@@ -1190,17 +1238,12 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(AttnArgs a, AttnPlan p
         m = mb;
     }
     const float L = m + logf(s);
-    acc *= 1.0f / s;
     char *orow = static_cast<char *>(a.o) +
                  ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
-    if constexpr (OUT_F32) {
-        *reinterpret_cast<f32x4 *>(orow + d * 4) = acc;
-    } else {
-        bf16x4 w;
-        for (int e = 0; e < 4; ++e) w[e] = (__bf16)acc[e];
-        *reinterpret_cast<bf16x4 *>(orow + d * 2) = w;
-    }
-    if (a.lse != nullptr && d == 0) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = L;
+    RunMerge w = out_row_weights<true>(a, b, h, qi, L);
+    w.wc *= 1.0f / s;
+    put_out4<OUT_F32>(a, orow, run_row<true>(a, b, h, qi), w, d, acc);
+    if (a.lse != nullptr && d == 0) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = w.lse;
 }
 
 // Chooses the work plan by a cost model in units of one key-tile iteration
@@ -1268,7 +1311,7 @@ hipMemPool_t workspace_pool()
         hipMemPool_t p = nullptr;
         if (hipMemPoolCreate(&p, &props) != hipSuccess) return nullptr;
         uint64_t keep = UINT64_MAX;
-        hipMemPoolSetAttribute(p, hipMemPoolAttrReleaseThreshold, &keep);
+        (void)hipMemPoolSetAttribute(p, hipMemPoolAttrReleaseThreshold, &keep);
         pools[dev] = p;
     }
     return pools[dev];
@@ -1303,10 +1346,17 @@ hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream)
     }
     const dim3 grid((unsigned)(pl.n_dp + pl.n_units)), block(kThreads);
     const int forced = forced_schedule();
-    if (forced == 1 || (forced == 0 && pl.n_kt >= kPingPongMinTiles))
-        hipLaunchKernelGGL((attn_fwd_pingpong_kernel<D, OUT_F32>), grid, block, 0, stream, a, pl);
-    else
-        hipLaunchKernelGGL((attn_fwd_kernel<D, OUT_F32>), grid, block, 0, stream, a, pl);
+    const bool pp = forced == 1 || (forced == 0 && pl.n_kt >= kPingPongMinTiles);
+    if (a.run_lse != nullptr) {
+        if (pp)
+            hipLaunchKernelGGL((attn_fwd_pingpong_kernel<D, OUT_F32, true>), grid, block, 0, stream, a, pl);
+        else
+            hipLaunchKernelGGL((attn_fwd_kernel<D, OUT_F32, true>), grid, block, 0, stream, a, pl);
+    } else if (pp) {
+        hipLaunchKernelGGL((attn_fwd_pingpong_kernel<D, OUT_F32, false>), grid, block, 0, stream, a, pl);
+    } else {
+        hipLaunchKernelGGL((attn_fwd_kernel<D, OUT_F32, false>), grid, block, 0, stream, a, pl);
+    }
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && pl.n_units > 0) {
         const int64_t threads = (int64_t)(pl.n_tiles - pl.n_dp) * BM * (D / 4);

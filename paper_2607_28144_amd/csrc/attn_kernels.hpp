@@ -22,6 +22,14 @@ struct AttnArgs {
     // K/V row offsets within a 64-key tile fit 31 bits (non-negative strides
     // below 2^24 elements): tile copies use a scalar base + 32-bit lane offsets
     bool kv_off32;
+    // Ring accumulate (run_lse set): run_o f32 [B,Sq,H,D] and run_lse hold
+    // the normalized output and LSE over the key chunks already seen; the
+    // epilogue merges this launch's result into them, writing O to o and the
+    // merged LSE to lse (== run_lse).  Rows whose run_lse is -inf have seen
+    // no key yet and do not read run_o.
+    const float *run_o;
+    float *run_lse;
+    int64_t r_sb, r_ss, r_sh;
 };
 
 // Work plan of one attention launch.  Query tiles [0, n_dp) are processed

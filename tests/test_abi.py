@@ -175,3 +175,38 @@ def test_norm_rope_in_place_passes_validation(lib):
     # exact aliasing of an output with its own input is allowed: validation
     # passes and the device query is what fails here
     expect(lib, norm_rope(lib, qo=T(FAKE), ko=T(FAKE + 0x1000000)), _lib.ERR_HIP, "hip")
+
+
+def ring(lib, q=None, k=None, v=None, run=None, lse=FAKE + 0x4000000, out=False, dtype=_lib.F32, B=1, H=2, Sq=64,
+         Skv=64, D=128, scale=0.088):
+    q = q if q is not None else T(FAKE, S=Sq, H=H, D=D)
+    k = k if k is not None else T(FAKE + 0x1000000, S=Skv, H=H, D=D)
+    v = v if v is not None else T(FAKE + 0x2000000, S=Skv, H=H, D=D)
+    run = run if run is not None else T(FAKE + 0x3000000, S=Sq, H=H, D=D)
+    byref = lambda t: ctypes.byref(t) if t is not False else None  # noqa: E731
+    return lib.regenvc_attn_ring_accumulate(byref(q), byref(k), byref(v), byref(run), lse, byref(out), dtype,
+                                            B, H, Sq, Skv, D, scale, None)
+
+
+def test_ring_accumulate_validation(lib):
+    expect(lib, ring(lib, run=False), _lib.ERR_INVALID_ARG, "o_run")
+    expect(lib, ring(lib, lse=None), _lib.ERR_INVALID_ARG, "required")
+    expect(lib, ring(lib, dtype=_lib.BF16), _lib.ERR_INVALID_ARG, "F32")      # o_run is f32: no bf16 write-back
+    expect(lib, ring(lib, Skv=0), _lib.ERR_INVALID_ARG, "key count")
+    expect(lib, ring(lib, D=96), _lib.ERR_UNSUPPORTED, "head dim")
+    expect(lib, ring(lib, run=T(FAKE + 0x3000008)), _lib.ERR_UNSUPPORTED, "aligned")
+    expect(lib, ring(lib, run=T(FAKE + 0x1000000)), _lib.ERR_INVALID_ARG, "overlaps")      # o_run on k
+    expect(lib, ring(lib, run=T(FAKE + 0x3000000, ss=0)), _lib.ERR_INVALID_ARG, "overlapping rows")
+    expect(lib, ring(lib, lse=FAKE + 0x3000000 + 64), _lib.ERR_INVALID_ARG, "overlaps")   # lse inside o_run
+    # a separate output must not overlap the running output unless it is that very view in f32
+    expect(lib, ring(lib, out=T(FAKE + 0x3000000 + 256), dtype=_lib.BF16), _lib.ERR_INVALID_ARG, "o_run")
+    expect(lib, ring(lib, out=T(FAKE + 0x3000000), dtype=_lib.BF16), _lib.ERR_INVALID_ARG, "o_run")
+    expect(lib, ring(lib, out=T(FAKE + 0x5000000), dtype=_lib.BF16, B=0), _lib.OK)
+    expect(lib, ring(lib, Sq=0), _lib.OK)
+
+
+@pytest.mark.skipif(has_gpu_node(), reason="would reach a launch on fake addresses on a GPU machine")
+def test_ring_accumulate_in_place_and_separate_output_pass_validation(lib):
+    expect(lib, ring(lib), _lib.ERR_HIP, "hip")
+    expect(lib, ring(lib, out=T(FAKE + 0x3000000), dtype=_lib.F32), _lib.ERR_HIP, "hip")
+    expect(lib, ring(lib, out=T(FAKE + 0x5000000), dtype=_lib.BF16), _lib.ERR_HIP, "hip")

@@ -252,6 +252,47 @@ def test_merge_empty_parts_have_weight_zero_and_all_empty_gives_zero_and_neg_inf
     assert np.all(oz == 0.0) and np.all(np.isneginf(lz))
 
 
+# ---------------------------------------------------------------- ring accumulate
+def _ring(q, k, v, scale, bounds):
+    """Ring steps over the chunks of `bounds`, from the no-key state (the
+    running output holds NaN: it must not be read)."""
+    B, Sq, H, D = q.shape
+    o = np.full((B, Sq, H, D), np.nan)
+    lse = np.full((B, H, Sq), -np.inf)
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        o, lse = oracle.ring_accumulate(o, lse, q, np.ascontiguousarray(k[:, a:b]),
+                                        np.ascontiguousarray(v[:, a:b]), scale)
+    return o, lse
+
+
+@pytest.mark.parametrize("bounds", [[0, 64, 128, 192, 256], [0, 1, 100, 101, 256], [0, 256]])
+def test_ring_steps_equal_unchunked_attention(bounds):
+    q, k, v = synth.qkv(19, 1, 2, 20, 256, 16)
+    scale = F32(0.25)
+    o, lse = oracle.attn(q, k, v, scale)
+    orr, lr = _ring(q, k, v, scale, bounds)
+    np.testing.assert_allclose(orr, o, rtol=0, atol=1e-13)
+    np.testing.assert_allclose(lr, lse, rtol=0, atol=1e-12)
+
+
+def test_ring_two_steps_match_brute_force_on_the_concatenated_keys():
+    rng = np.random.default_rng(20)
+    q, k, v = (ints_bf16(rng, s, -3, 3) for s in [(1, 3, 2, 4), (1, 7, 2, 4), (1, 7, 2, 4)])
+    scale = F32(0.5)
+    ob, lb = brute.attn(q, k, v, float(scale))
+    orr, lr = _ring(q, k, v, scale, [0, 3, 7])
+    np.testing.assert_allclose(orr, np.array(ob), rtol=0, atol=1e-13)
+    np.testing.assert_allclose(lr, np.array(lb), rtol=0, atol=1e-13)
+
+
+def test_ring_step_from_no_keys_is_the_chunk_result_and_ignores_the_running_output():
+    q, k, v = synth.qkv(21, 1, 2, 6, 40, 8)
+    scale = F32(0.3)
+    o, lse = oracle.attn(q, k, v, scale)
+    orr, lr = _ring(q, k, v, scale, [0, 40])
+    assert np.array_equal(orr, o) and np.array_equal(lr, lse)
+
+
 # ---------------------------------------------------------------- planted mistakes
 # Plausible slips in the oracle, planted in a copy of its source; each must
 # make at least one pin fail.
