@@ -155,11 +155,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=20, help="untimed steps (the clock settles under load)")
-    ap.add_argument("--only", choices=["self", "cross", "share", "copy", "normrope"], default=None,
+    ap.add_argument("--only", choices=["self", "cross", "share", "ring", "copy", "normrope"], default=None,
                     help="time one component alone (for profiling); 'copy' runs a plain 1 GiB elementwise "
                          "copy kernel, the reference for scaling HBM byte counters; 'normrope' times the q/k "
                          "RMSNorm + 3D rotary embedding that produces the window's attention inputs (not part "
-                         "of the attention step)")
+                         "of the attention step); 'ring' runs the share with the merge fused into each chunk "
+                         "(first chunk's partial, then ring-accumulate steps, the last into bf16)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle sample")
     args = ap.parse_args()
@@ -210,6 +211,7 @@ def main():
         "self": attn_flops(B, H, S, S, D),
         "cross": attn_flops(B, H, S, W["ctx"], D),
         "share": attn_flops(R["B"], R["H"], R["S"], R["S"], R["D"]),
+        "ring": attn_flops(R["B"], R["H"], R["S"], R["S"], R["D"]),
     }
     stream = torch.cuda.current_stream(dev)
     ev = {c: [] for c in comps}
@@ -223,11 +225,18 @@ def main():
                 api.attn_fwd(q, k, v, scale=scale, out=o_self, lse_out=l_self)
             elif c == "cross":
                 api.cross_attn_fwd(q, kc, vc, scale=scale, out=o_cross, lse_out=l_cross)
-            else:
+            elif c == "share":
                 for i in range(nch):
                     a, b = bounds[i], bounds[i + 1]
                     api.attn_partial_fwd(rq, rk[:, a:b], rv[:, a:b], scale=scale, out=o_parts[i], lse_out=l_parts[i])
                 api.lse_merge(o_parts, l_parts, out=o_share, lse_out=l_share)
+            else:  # the same share with the merge fused into each chunk's epilogue
+                api.attn_partial_fwd(rq, rk[:, :bounds[1]], rv[:, :bounds[1]], scale=scale, out=o_parts[0],
+                                     lse_out=l_parts[0])
+                for i in range(1, nch):
+                    a, b = bounds[i], bounds[i + 1]
+                    api.attn_ring_accumulate(rq, rk[:, a:b], rv[:, a:b], o_parts[0], l_parts[0], scale=scale,
+                                             out=o_share if i == nch - 1 else None, out_dtype=torch.bfloat16)
             if record:
                 e1 = torch.cuda.Event(enable_timing=True)
                 e1.record(stream)

@@ -149,9 +149,10 @@ regenvc_status regenvc_lse_merge(const float *const *o_parts,
    (O_c, L_c) the chunk's normalized result and LSE:
      L = log(exp L_run + exp L_c);  O = exp(L_run - L) O_run + exp(L_c - L) O_c
    (the regenvc_lse_merge identity for two parts).
-     o_run: f32 [B,Sq,H,D], the normalized output over the chunks so far;
-       read only where lse_run is finite (a row with lse_run = -inf has seen
-       no key and its o_run may hold anything)
+     o_run: f32 [B,Sq,H,D], the normalized output over the chunks so far
+       (the whole view must be valid memory); where lse_run is -inf the row
+       has seen no key and its o_run values are ignored (they may hold
+       anything, NaN included)
      lse_run: f32 [B,H,Sq], required; read, then overwritten in place with L
      o_out: NULL writes O back into o_run (f32, o_dtype must be
        REGENVC_F32); otherwise O goes to o_out in o_dtype (bf16 or f32, e.g.

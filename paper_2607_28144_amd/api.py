@@ -94,7 +94,7 @@ def attn_ring_accumulate(q: torch.Tensor, k_chunk: torch.Tensor, v_chunk: torch.
                          out_dtype: torch.dtype = torch.float32) -> torch.Tensor:
     """Partial attention over one key/value chunk merged into the running
     state (regenvc_attn_ring_accumulate).  o_run: float32 [B, Sq, H, D]
-    normalized output so far (not read where lse_run is -inf); lse_run:
+    normalized output so far (ignored where lse_run is -inf); lse_run:
     float32 [B, H, Sq], updated in place.  With out=None the merged output
     goes back into o_run; otherwise into `out` (out_dtype).  Returns the
     tensor that holds the merged output."""

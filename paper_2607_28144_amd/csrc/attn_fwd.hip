@@ -294,7 +294,8 @@ __device__ __forceinline__ WorkItem work_item(const AttnPlan &pl, int item)
 // chunks seen so far, and its LSE L_run) and this launch's normalized result
 // (O_c, L_c) combine, by the log-sum-exp identity of the chunk merge:
 // L = log(e^L_run + e^L_c), O = e^(L_run - L) O_run + e^(L_c - L) O_c.  A row
-// with L_run = -inf has seen no key: O_run is not read (it may hold anything).
+// with L_run = -inf has seen no key: its O_run values (anything, NaN
+// included) do not enter the result.
 struct RunMerge {
     float wr, wc, lse;
     bool run;  // O_run enters the result
@@ -318,23 +319,14 @@ __device__ __forceinline__ RunMerge run_merge(float lr, float lc)
     return m;
 }
 
-// Output row of query qi of (b, h) and, in the ring-accumulate mode, the
-// merge weights of that row (w.wc multiplies this launch's normalized O).
-template <bool ACC>
-__device__ __forceinline__ RunMerge out_row_weights(const AttnArgs &a, int b, int h, int qi, float lse_c)
-{
-    if (!ACC || a.run_lse == nullptr) return RunMerge{0.f, 1.f, lse_c, false};
-    return run_merge(a.run_lse[((int64_t)b * a.H + h) * a.Sq + qi], lse_c);
-}
-
-// Four consecutive output values of a row: w.wc * oc (+ w.wr * O_run when the
-// running state enters), stored as f32 or bf16 at element d of the row.
+// Four consecutive output values of a row: w.wc * oc (+ w.wr * run, the
+// running output's values, when the running state enters), stored as f32 or
+// bf16 at element d of the row.
 template <bool OUT_F32>
-__device__ __forceinline__ void put_out4(const AttnArgs &a, char *orow, const float *rrow, const RunMerge &w, int d,
-                                         f32x4 oc)
+__device__ __forceinline__ void put_out4(char *orow, const RunMerge &w, int d, f32x4 oc, f32x4 run)
 {
     f32x4 r = oc * w.wc;
-    if (w.run) r += *reinterpret_cast<const f32x4 *>(rrow + d) * w.wr;
+    if (w.run) r += run * w.wr;
     if constexpr (OUT_F32) {
         *reinterpret_cast<f32x4 *>(orow + d * 4) = r;
     } else {
@@ -345,10 +337,19 @@ __device__ __forceinline__ void put_out4(const AttnArgs &a, char *orow, const fl
     }
 }
 
-template <bool ACC>
-__device__ __forceinline__ const float *run_row(const AttnArgs &a, int b, int h, int qi)
+// The running state of row qi (clamped into the sequence, so that a padded
+// query row reads a real row it then ignores): LSE and the f32x4 chunks at
+// d = d0 + j * dstep of the running output, all loaded before any output is
+// written (the output may be the running output itself, so a store must not
+// come between them).
+template <int N>
+__device__ __forceinline__ float load_run(const AttnArgs &a, int b, int h, int qi, int d0, int dstep, f32x4 (&run)[N])
 {
-    return !ACC || a.run_o == nullptr ? nullptr : a.run_o + ((int64_t)b * a.r_sb + (int64_t)qi * a.r_ss + (int64_t)h * a.r_sh);
+    qi = min(qi, a.Sq - 1);
+    const float *rrow = a.run_o + ((int64_t)b * a.r_sb + (int64_t)qi * a.r_ss + (int64_t)h * a.r_sh);
+#pragma unroll
+    for (int j = 0; j < N; ++j) run[j] = *reinterpret_cast<const f32x4 *>(rrow + d0 + j * dstep);
+    return a.run_lse[((int64_t)b * a.H + h) * a.Sq + qi];
 }
 
 // Epilogue of one lane's query row: O = O^T / l and LSE = ln2 * (m_ref +
@@ -381,9 +382,10 @@ __device__ __forceinline__ void store_row(const AttnArgs &a, const AttnPlan &pl,
     } else {
         char *orow = static_cast<char *>(a.o) +
                      ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
-        RunMerge w = out_row_weights<ACC>(a, b, h, qi, lse_val);
+        f32x4 run[ACC ? DB * 4 : 1] = {};
+        RunMerge w{0.f, 1.f, lse_val, false};
+        if constexpr (ACC) w = run_merge(load_run(a, b, h, qi, hi * 4, 8, run), lse_val);
         w.wc *= inv;
-        const float *rrow = run_row<ACC>(a, b, h, qi);
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -391,7 +393,7 @@ __device__ __forceinline__ void store_row(const AttnArgs &a, const AttnPlan &pl,
                 f32x4 oc;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) oc[e] = oacc[db][gq * 4 + e];
-                put_out4<OUT_F32>(a, orow, rrow, w, db * 32 + gq * 8 + hi * 4, oc);
+                put_out4<OUT_F32>(orow, w, db * 32 + gq * 8 + hi * 4, oc, run[ACC ? db * 4 + gq : 0]);
             }
         if (a.lse != nullptr && hi == 0) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = w.lse;
     }
@@ -1156,6 +1158,16 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     // Epilogue: per query, l = the sum of the four lanes' partial sums;
     // O = O^T / l, LSE = ln2 * (m_ref + log2 l); a split tile's key range
     // writes its normalized partial to the workspace instead.
+    // In the ring-accumulate mode the running state of both rows is loaded
+    // first, in one batch.
+    f32x4 run[2][ACC ? DB : 1] = {};
+    float run_l[2] = {-INFINITY, -INFINITY};
+    if constexpr (ACC) {
+        if (slot < 0) {
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb) run_l[qb] = load_run(a, b, h, qi0 + qb * 16, g * 4, 16, run[qb]);
+        }
+    }
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
         const float lt = quad_sum(lsum[qb]);
@@ -1176,11 +1188,12 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
         } else {
             char *orow = static_cast<char *>(a.o) +
                          ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
-            RunMerge w = out_row_weights<ACC>(a, b, h, qi, lse_val);
+            RunMerge w{0.f, 1.f, lse_val, false};
+            if constexpr (ACC) w = run_merge(run_l[qb], lse_val);
             w.wc *= inv;
-            const float *rrow = run_row<ACC>(a, b, h, qi);
 #pragma unroll
-            for (int db = 0; db < DB; ++db) put_out4<OUT_F32>(a, orow, rrow, w, db * 16 + g * 4, oacc[db][qb]);
+            for (int db = 0; db < DB; ++db)
+                put_out4<OUT_F32>(orow, w, db * 16 + g * 4, oacc[db][qb], run[qb][ACC ? db : 0]);
             if (a.lse != nullptr && g == 0) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = w.lse;
         }
     }
@@ -1240,9 +1253,11 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(AttnArgs a, AttnPlan p
     const float L = m + logf(s);
     char *orow = static_cast<char *>(a.o) +
                  ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
-    RunMerge w = out_row_weights<true>(a, b, h, qi, L);
+    RunMerge w{0.f, 1.f, L, false};
+    f32x4 run[1] = {};
+    if (a.run_lse != nullptr) w = run_merge(load_run(a, b, h, qi, d, 0, run), L);
     w.wc *= 1.0f / s;
-    put_out4<OUT_F32>(a, orow, run_row<true>(a, b, h, qi), w, d, acc);
+    put_out4<OUT_F32>(orow, w, d, acc, run[0]);
     if (a.lse != nullptr && d == 0) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = w.lse;
 }
 

@@ -26,7 +26,7 @@ struct AttnArgs {
     // the normalized output and LSE over the key chunks already seen; the
     // epilogue merges this launch's result into them, writing O to o and the
     // merged LSE to lse (== run_lse).  Rows whose run_lse is -inf have seen
-    // no key yet and do not read run_o.
+    // no key yet: their run_o values are ignored.
     const float *run_o;
     float *run_lse;
     int64_t r_sb, r_ss, r_sh;
