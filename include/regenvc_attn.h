@@ -12,7 +12,8 @@
  *                               or regenvc_attn_ring_accumulate (merge fused)
  *   - the conditioning path (Sec. 3.9, "Hybrid CPU-GPU deployment") streams
  *     precomputed text/image key/value tensors to the GPU, which the video
- *     tokens cross-attend to                         -> regenvc_cross_attn_fwd
+ *     tokens cross-attend to                         -> regenvc_cross_attn_fwd,
+ *     both contexts summed with Q read once         -> regenvc_cross_attn_dual_fwd
  *
  * Definition (per batch b, head h, query row i; scale = softmax_scale):
  *     s_j = scale * <Q[b,i,h,:], K[b,j,h,:]>,  j = 0..Skv-1
@@ -181,6 +182,29 @@ regenvc_status regenvc_cross_attn_fwd(const regenvc_tensor *q,
                                       float *lse, int32_t B, int32_t H, int32_t Sq,
                                       int32_t Sctx, int32_t D, float softmax_scale,
                                       void *stream);
+
+/* Dual cross-attention: the video tokens attend to the text context (T5
+   tokens) and, separately, to the image context (CLIP tokens), and the two
+   results are summed -- the two conditioning streams whose key/value tensors
+   Sec. 3.9 precomputes off-GPU.  Per row:
+     O = softmax(scale Q K_txt^T) V_txt + softmax(scale Q K_img^T) V_img
+   Each softmax is over its own context (not a joint softmax over both).  Q
+   is read once: one kernel runs the key pipeline over the text context,
+   keeps that normalized result on chip in bf16 (the precision of a single
+   cross-attention output), then runs the image context and adds.
+     k_txt/v_txt: bf16 [B,S_txt,H,D]; k_img/v_img: bf16 [B,S_img,H,D]
+     o: bf16 [B,Sq,H,D] (bf16 only: o_dtype is implied)
+     lse_txt, lse_img: f32 [B,H,Sq] LSE of each context's softmax, or NULL
+   S_txt and S_img must be >= 1.  Other rules as regenvc_attn_fwd. */
+regenvc_status regenvc_cross_attn_dual_fwd(const regenvc_tensor *q,
+                                           const regenvc_tensor *k_txt,
+                                           const regenvc_tensor *v_txt, int32_t S_txt,
+                                           const regenvc_tensor *k_img,
+                                           const regenvc_tensor *v_img, int32_t S_img,
+                                           const regenvc_tensor *o, float *lse_txt,
+                                           float *lse_img, int32_t B, int32_t H,
+                                           int32_t Sq, int32_t D, float softmax_scale,
+                                           void *stream);
 
 /* q/k RMSNorm + 3D rotary position embedding: the steps that turn the QKV
    projection's q and k into the attention inputs in a block of the video

@@ -101,6 +101,16 @@ def ring_accumulate(o_run, lse_run, q, k, v, scale: float, lib=None):
     return merge([o_run, o_c], [lse_run, l_c], lib)
 
 
+def cross_attn_dual(q, k_txt, v_txt, k_img, v_img, scale: float, lib=None):
+    """Text and image cross-attention summed (paper Sec. 3.9: the video tokens
+    are conditioned on both the T5 text and the CLIP image key/values): each
+    context has its own softmax, and the two outputs are added.  Returns
+    (O float64 [B,Sq,H,D], LSE_txt, LSE_img float64 [B,H,Sq])."""
+    o_t, l_t = attn(q, k_txt, v_txt, scale, lib)
+    o_i, l_i = attn(q, k_img, v_img, scale, lib)
+    return o_t + o_i, l_t, l_i
+
+
 def norm_rope(x: np.ndarray, w: np.ndarray, grid, token0: int = 0, eps: float = 1e-6, theta: float = 10000.0,
               lib=None):
     """q or k RMSNorm over all H*D channels of a token, then 3D rotary

@@ -9,7 +9,8 @@ a C ABI (include/regenvc_attn.h).  Import is cheap: the library and torch are
 loaded on first use.
 """
 
-__all__ = ["attn_fwd", "attn_partial_fwd", "lse_merge", "attn_ring_accumulate", "cross_attn_fwd", "attn_plan", "qk_norm_rope",
+__all__ = ["attn_fwd", "attn_partial_fwd", "lse_merge", "attn_ring_accumulate", "cross_attn_fwd",
+           "cross_attn_dual_fwd", "attn_plan", "qk_norm_rope",
            "RegenvcError"]
 
 

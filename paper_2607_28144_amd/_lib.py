@@ -42,6 +42,8 @@ _SIGNATURES = {
                           _PT, ctypes.c_int, ctypes.c_void_p, _i32, _i32, _i32, _i32, ctypes.c_void_p],
     "regenvc_attn_ring_accumulate": [_PT, _PT, _PT, _PT, ctypes.c_void_p, _PT, ctypes.c_int,
                                      _i32, _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_void_p],
+    "regenvc_cross_attn_dual_fwd": [_PT, _PT, _PT, _i32, _PT, _PT, _i32, _PT, ctypes.c_void_p, ctypes.c_void_p,
+                                    _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_void_p],
     "regenvc_cross_attn_fwd": [_PT, _PT, _PT, _PT, ctypes.c_int, ctypes.c_void_p,
                                _i32, _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_void_p],
     "regenvc_attn_plan_query": [_i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(AttnPlan)],

@@ -132,6 +132,36 @@ def cross_attn_fwd(q: torch.Tensor, k_ctx: torch.Tensor, v_ctx: torch.Tensor, sc
     return _attn("regenvc_cross_attn_fwd", q, k_ctx, v_ctx, scale, out_dtype, out, return_lse, lse_out)
 
 
+def cross_attn_dual_fwd(q: torch.Tensor, k_txt: torch.Tensor, v_txt: torch.Tensor, k_img: torch.Tensor,
+                        v_img: torch.Tensor, scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
+                        return_lse: bool = True, lse_txt: Optional[torch.Tensor] = None,
+                        lse_img: Optional[torch.Tensor] = None):
+    """Text and image cross-attention summed, Q read once
+    (regenvc_cross_attn_dual_fwd).  Returns (O bf16, LSE_txt, LSE_img) -- the
+    LSEs None unless return_lse or given."""
+    B, Sq, H, D = q.shape
+    St, Si = k_txt.shape[1], k_img.shape[1]
+    for name, t, S in [("k_txt", k_txt, St), ("v_txt", v_txt, St), ("k_img", k_img, Si), ("v_img", v_img, Si)]:
+        if tuple(t.shape) != (B, S, H, D):
+            raise ValueError(f"{name} shape {tuple(t.shape)} does not match q {tuple(q.shape)}")
+    if out is None:
+        out = torch.empty((B, Sq, H, D), dtype=torch.bfloat16, device=q.device)
+    if return_lse:
+        lse_txt = lse_txt if lse_txt is not None else torch.empty((B, H, Sq), dtype=torch.float32, device=q.device)
+        lse_img = lse_img if lse_img is not None else torch.empty((B, H, Sq), dtype=torch.float32, device=q.device)
+    descs = [_desc(t, n, torch.bfloat16) for t, n in
+             [(q, "q"), (k_txt, "k_txt"), (v_txt, "v_txt"), (k_img, "k_img"), (v_img, "v_img"), (out, "out")]]
+    lt, li = _fptr(lse_txt, "lse_txt", (B, H, Sq)), _fptr(lse_img, "lse_img", (B, H, Sq))
+    lib = _lib.load()
+    with torch.cuda.device(q.device):
+        st = lib.regenvc_cross_attn_dual_fwd(ctypes.byref(descs[0]), ctypes.byref(descs[1]), ctypes.byref(descs[2]),
+                                             St, ctypes.byref(descs[3]), ctypes.byref(descs[4]), Si,
+                                             ctypes.byref(descs[5]), lt, li, B, H, Sq, D, _scale(scale, D),
+                                             _stream(q.device))
+    _lib.check(st, "regenvc_cross_attn_dual_fwd")
+    return out, lse_txt, lse_img
+
+
 def lse_merge(o_parts: Sequence[torch.Tensor], lse_parts: Sequence[torch.Tensor],
               out_dtype: torch.dtype = torch.bfloat16, out: Optional[torch.Tensor] = None,
               return_lse: bool = True, lse_out: Optional[torch.Tensor] = None

@@ -156,12 +156,21 @@ bool same_view(const regenvc_tensor *a, const regenvc_tensor *b)
     return a->ptr == b->ptr && a->stride_b == b->stride_b && a->stride_s == b->stride_s && a->stride_h == b->stride_h;
 }
 
+// Second context of a dual cross-attention.
+struct Ctx2 {
+    const regenvc_tensor *k, *v;
+    int32_t S;
+    float *lse;  // may be null
+};
+
 // run_o (ring accumulate only): f32 running output, read; lse is then the
 // running LSE, read and rewritten in place; o may be run_o itself (f32).
+// ctx2 (dual cross-attention only): the second context, summed into o.
 regenvc_status attn_common(const char *fn, const regenvc_tensor *q, const regenvc_tensor *k,
                            const regenvc_tensor *v, const regenvc_tensor *o, regenvc_dtype o_dtype, float *lse,
                            bool lse_required, int32_t B, int32_t H, int32_t Sq, int32_t Skv, int32_t D, float scale,
-                           void *stream, bool allow_empty_keys, const regenvc_tensor *run_o = nullptr)
+                           void *stream, bool allow_empty_keys, const regenvc_tensor *run_o = nullptr,
+                           const Ctx2 *ctx2 = nullptr)
 {
     regenvc_status st = check_sizes(B, H, Sq, D);
     if (st != REGENVC_OK) return st;
@@ -171,11 +180,19 @@ regenvc_status attn_common(const char *fn, const regenvc_tensor *q, const regenv
         return fail(REGENVC_ERR_INVALID_ARG, "%s: unknown output dtype %d", fn, (int)o_dtype);
     if ((st = check_scale(scale)) != REGENVC_OK) return st;
     if (lse_required && lse == nullptr) return fail(REGENVC_ERR_INVALID_ARG, "%s: lse output is required", fn);
+    if (ctx2 != nullptr) {
+        if (ctx2->S < 1) return fail(REGENVC_ERR_INVALID_ARG, "%s: second context length %d must be >= 1", fn, ctx2->S);
+        if (o_dtype != REGENVC_BF16)
+            return fail(REGENVC_ERR_UNSUPPORTED, "%s: the summed output is bf16 only (o_dtype must be BF16)", fn);
+        if (ctx2->lse != nullptr && reinterpret_cast<uintptr_t>(ctx2->lse) % 4 != 0)
+            return fail(REGENVC_ERR_UNSUPPORTED, "%s: lse_img pointer is not 4-byte aligned", fn);
+    }
     if (lse != nullptr && reinterpret_cast<uintptr_t>(lse) % 4 != 0)
         return fail(REGENVC_ERR_UNSUPPORTED, "%s: lse pointer is not 4-byte aligned", fn);
     if (B == 0 || H == 0 || Sq == 0) {
         // empty problem: nothing to read or write, but descriptors must still be present
-        if (!q || !k || !v || !o) return fail(REGENVC_ERR_INVALID_ARG, "%s: descriptor is NULL", fn);
+        if (!q || !k || !v || !o || (ctx2 && (!ctx2->k || !ctx2->v)))
+            return fail(REGENVC_ERR_INVALID_ARG, "%s: descriptor is NULL", fn);
         g_last_error[0] = '\0';
         return REGENVC_OK;
     }
@@ -198,6 +215,24 @@ regenvc_status attn_common(const char *fn, const regenvc_tensor *q, const regenv
         const Extent el = flat_extent(lse, (int64_t)B * H * Sq, 4);
         if (overlap(el, eq) || overlap(el, eo) || (Skv > 0 && (overlap(el, ek) || overlap(el, ev))))
             return fail(REGENVC_ERR_INVALID_ARG, "%s: lse overlaps another tensor", fn);
+    }
+    if (ctx2 != nullptr) {
+        Extent ek2, ev2;
+        if ((st = check_view("k_img", ctx2->k, B, ctx2->S, H, D, 2, &ek2)) != REGENVC_OK) return st;
+        if ((st = check_view("v_img", ctx2->v, B, ctx2->S, H, D, 2, &ev2)) != REGENVC_OK) return st;
+        if (overlap(eo, ek2) || overlap(eo, ev2))
+            return fail(REGENVC_ERR_INVALID_ARG, "%s: output o overlaps an input", fn);
+        if (lse != nullptr) {
+            const Extent el = flat_extent(lse, (int64_t)B * H * Sq, 4);
+            if (overlap(el, ek2) || overlap(el, ev2))
+                return fail(REGENVC_ERR_INVALID_ARG, "%s: lse overlaps another tensor", fn);
+        }
+        if (ctx2->lse != nullptr) {
+            const Extent el2 = flat_extent(ctx2->lse, (int64_t)B * H * Sq, 4);
+            if (overlap(el2, eq) || overlap(el2, ek) || overlap(el2, ev) || overlap(el2, ek2) || overlap(el2, ev2) ||
+                overlap(el2, eo) || (lse != nullptr && overlap(el2, flat_extent(lse, (int64_t)B * H * Sq, 4))))
+                return fail(REGENVC_ERR_INVALID_ARG, "%s: lse_img overlaps another tensor", fn);
+        }
     }
     if (run_o != nullptr) {
         Extent er;
@@ -244,6 +279,15 @@ regenvc_status attn_common(const char *fn, const regenvc_tensor *q, const regenv
     a.o_f32 = o_dtype == REGENVC_F32;
     a.scale = scale;
     a.kv_off32 = k->stride_s >= 0 && v->stride_s >= 0 && k->stride_s < (1 << 24) && v->stride_s < (1 << 24);
+    if (ctx2 != nullptr) {
+        a.k2 = ctx2->k->ptr;
+        a.v2 = ctx2->v->ptr;
+        a.lse2 = ctx2->lse;
+        a.k2_sb = ctx2->k->stride_b, a.k2_ss = ctx2->k->stride_s, a.k2_sh = ctx2->k->stride_h;
+        a.v2_sb = ctx2->v->stride_b, a.v2_ss = ctx2->v->stride_s, a.v2_sh = ctx2->v->stride_h;
+        a.Skv2 = ctx2->S;
+        a.kv2_off32 = a.k2_ss >= 0 && a.v2_ss >= 0 && a.k2_ss < (1 << 24) && a.v2_ss < (1 << 24);
+    }
     if (run_o != nullptr) {
         a.run_o = static_cast<const float *>(run_o->ptr);
         a.run_lse = lse;
@@ -295,6 +339,17 @@ regenvc_status regenvc_cross_attn_fwd(const regenvc_tensor *q, const regenvc_ten
 {
     return attn_common("regenvc_cross_attn_fwd", q, k_ctx, v_ctx, o, o_dtype, lse, false, B, H, Sq, Sctx, D,
                        softmax_scale, stream, false);
+}
+
+regenvc_status regenvc_cross_attn_dual_fwd(const regenvc_tensor *q, const regenvc_tensor *k_txt,
+                                           const regenvc_tensor *v_txt, int32_t S_txt, const regenvc_tensor *k_img,
+                                           const regenvc_tensor *v_img, int32_t S_img, const regenvc_tensor *o,
+                                           float *lse_txt, float *lse_img, int32_t B, int32_t H, int32_t Sq, int32_t D,
+                                           float softmax_scale, void *stream)
+{
+    const Ctx2 c2{k_img, v_img, S_img, lse_img};
+    return attn_common("regenvc_cross_attn_dual_fwd", q, k_txt, v_txt, o, REGENVC_BF16, lse_txt, false, B, H, Sq, S_txt,
+                       D, softmax_scale, stream, false, nullptr, &c2);
 }
 
 regenvc_status regenvc_lse_merge(const float *const *o_parts, const float *const *lse_parts, int32_t num_parts,

@@ -261,6 +261,16 @@ __device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, flo
     lsum = fmaf(lsum, alpha, acc0 + acc1);
 }
 
+// One key/value context of a (batch, head): K and V base pointers, row
+// strides (elements), length, key tiles, and whether tile copies can use
+// 32-bit lane offsets.
+struct KvSrc {
+    const uint16_t *k, *v;
+    int64_t k_ss, v_ss;
+    int Skv, n_kt;
+    bool off32;
+};
+
 // Work item of a workgroup: one key range of a split tile (the first
 // n_units workgroups, so that these short items start with the first round
 // instead of trailing the last one) or a whole query tile.  Whole tiles are
@@ -269,15 +279,24 @@ __device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, flo
 // contiguous range of tiles so that one head's tiles share an L2.
 struct WorkItem {
     int tile, kt0, kt1, slot;  // slot: workspace row block of a key range, -1 for a whole tile
+    int src;                   // context of a key range (dual launches: 1 = the second)
 };
 __device__ __forceinline__ WorkItem work_item(const AttnPlan &pl, int item)
 {
     WorkItem w;
+    w.src = 0;
     if (item < pl.n_units) {
-        const int sgi = item % pl.seg;
-        w.tile = pl.n_dp + item / pl.seg;
-        w.kt0 = (int)((int64_t)sgi * pl.n_kt / pl.seg);
-        w.kt1 = (int)((int64_t)(sgi + 1) * pl.n_kt / pl.seg);
+        const int per = pl.seg + pl.seg2;
+        int sgi = item % per, seg = pl.seg, nkt = pl.n_kt;
+        if (sgi >= pl.seg) {
+            sgi -= pl.seg;
+            seg = pl.seg2;
+            nkt = pl.n_kt2;
+            w.src = 1;
+        }
+        w.tile = pl.n_dp + item / per;
+        w.kt0 = (int)((int64_t)sgi * nkt / seg);
+        w.kt1 = (int)((int64_t)(sgi + 1) * nkt / seg);
         w.slot = item;
     } else {
         const int j = item - pl.n_units;
@@ -405,9 +424,12 @@ __device__ __forceinline__ void wait_vmcnt()
     __asm__ volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
 }
 
-// ACC: the ring-accumulate epilogue (a separate instantiation, so that the
-// plain kernels keep their register allocation).
-template <int D, bool OUT_F32, bool ACC>
+// ACC: the ring-accumulate epilogue; DUAL: two contexts summed (each a
+// separate instantiation, so that the plain kernels keep their register
+// allocation).  A dual launch runs the key pipeline twice over one set of Q
+// fragments: first context, then, with the first result parked in LDS as
+// bf16 (the precision of a single context-attention output), the second.
+template <int D, bool OUT_F32, bool ACC, bool DUAL = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 {
@@ -416,7 +438,9 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     constexpr int BM = kWaves * 32;
     constexpr int PER_TILE = 2 * LOADS;  // copies in flight per thread per tile (K and V)
 
-    __shared__ __attribute__((aligned(1024))) char smem[G::LDS];
+    // dual launches: + the first context's normalized O (bf16), 16-byte chunk
+    // j of thread t at byte G::LDS + 16 * (j * kThreads + t)
+    __shared__ __attribute__((aligned(1024))) char smem[G::LDS + (DUAL ? BM * D * 2 : 0)];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
@@ -424,7 +448,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     const int col = lane & 31;  // query column owned in the 32x32 accumulators
 
     const WorkItem wi = work_item(pl, blockIdx.x);
-    const int tile = wi.tile, kt0 = wi.kt0, kt1 = wi.kt1, slot = wi.slot;
+    const int tile = wi.tile, slot = wi.slot;
     const int qt = tile % pl.n_qtiles;
     const int bh = tile / pl.n_qtiles;
     const int h = bh % a.H;
@@ -433,11 +457,11 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     const int qi = qt * BM + qrow;     // ... and in the sequence
 
     const uint16_t *qp = static_cast<const uint16_t *>(a.q) + b * a.q_sb + h * a.q_sh;
-    const uint16_t *kp = static_cast<const uint16_t *>(a.k) + b * a.k_sb + h * a.k_sh;
-    const uint16_t *vp = static_cast<const uint16_t *>(a.v) + b * a.v_sb + h * a.v_sh;
-    const int Sq = a.Sq, Skv = a.Skv;
-    // only the last key tile of the whole sequence can be ragged
-    const bool ragged_end = kt1 == pl.n_kt && (Skv % kBlockN) != 0;
+    const int Sq = a.Sq;
+    // key/value contexts of this (b, h)
+    const KvSrc src0{static_cast<const uint16_t *>(a.k) + b * a.k_sb + h * a.k_sh,
+                     static_cast<const uint16_t *>(a.v) + b * a.v_sb + h * a.v_sh,
+                     a.k_ss, a.v_ss, a.Skv, pl.n_kt, a.kv_off32};
 
     // Q^T operand fragments stay in registers for the whole key loop.
     bf16x8 qf[DS];
@@ -448,6 +472,28 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         else
             qf[ds] = bf16x8{};
     }
+
+    const KvSrc src1 = DUAL ? KvSrc{static_cast<const uint16_t *>(a.k2) + b * a.k2_sb + h * a.k2_sh,
+                                    static_cast<const uint16_t *>(a.v2) + b * a.v2_sb + h * a.v2_sh,
+                                    a.k2_ss, a.v2_ss, a.Skv2, pl.n_kt2, a.kv2_off32}
+                            : src0;
+    f32x16 oacc[DB];
+    float mref, lsum;
+    const float c = a.scale * kLog2e;
+    float lse1 = 0.f;  // dual launches: LSE of the first context
+
+    // Passes of the key pipeline, each from the empty state into (oacc, mref,
+    // lsum): one over the work item's key range, or (dual launches, whole
+    // tiles) one over each context.
+    const int n_pass = DUAL && slot < 0 ? 2 : 1;
+    for (int ps = 0; ps < n_pass; ++ps) {
+    const KvSrc src = (DUAL && (slot >= 0 ? wi.src : ps) == 1) ? src1 : src0;
+    const int kt0 = wi.kt0;
+    const int kt1 = DUAL && slot < 0 ? src.n_kt : wi.kt1;
+    const uint16_t *kp = src.k, *vp = src.v;
+    const int Skv = src.Skv;
+    // only the last key tile of the whole context can be ragged
+    const bool ragged_end = kt1 == src.n_kt && (Skv % kBlockN) != 0;
 
     // HBM -> LDS copy of one key tile into a ring stage.  Each wave
     // instruction fills 1 KB of LDS (64 lanes x 16 B, in lane order); the
@@ -462,13 +508,13 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     for (int j = 0; j < LOADS; ++j) {
         const int slot16 = (wave * LOADS + j) * 64 + lane;
         const int row = slot16 / NCH, phys = slot16 % NCH;
-        kofs[j] = (uint32_t)((row * a.k_ss + k_slot<NCH>(row, phys) * 8) * 2);
-        vofs[j] = (uint32_t)((row * a.v_ss + v_slot<NCH>(row, phys) * 8) * 2);
+        kofs[j] = (uint32_t)((row * src.k_ss + k_slot<NCH>(row, phys) * 8) * 2);
+        vofs[j] = (uint32_t)((row * src.v_ss + v_slot<NCH>(row, phys) * 8) * 2);
     }
     // Tiles are copied in order kt0, kt0+1, ... (one call per tile); the
     // scalar source bases advance by one tile per call and stay on the last
     // tile once it is reached.  `stage` is the ring stage to fill.
-    const int64_t k_step = (int64_t)kBlockN * a.k_ss, v_step = (int64_t)kBlockN * a.v_ss;
+    const int64_t k_step = (int64_t)kBlockN * src.k_ss, v_step = (int64_t)kBlockN * src.v_ss;
     const int last_full = Skv / kBlockN - 1;  // last tile with kBlockN keys
     int tl_copy = kt0;
     const uint16_t *kb_copy = kp + kt0 * k_step;
@@ -476,7 +522,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     auto issue_next = [&](int stage) {
         const uint32_t kdst = lds0 + stage * G::STAGE;
         const uint32_t vdst = kdst + G::TILE;
-        if (a.kv_off32 && tl_copy <= last_full) {
+        if (src.off32 && tl_copy <= last_full) {
             // full tile: scalar tile base + precomputed 32-bit lane offsets
 #pragma unroll
             for (int j = 0; j < LOADS; ++j) {
@@ -493,8 +539,8 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
                 const int slot16 = blk * 64 + lane;
                 const int row = slot16 / NCH, phys = slot16 % NCH;
                 const int64_t key = key0 + min(row, last);
-                lds_dma16(kp + key * a.k_ss + k_slot<NCH>(row, phys) * 8, kdst + blk * 1024);
-                lds_dma16(vp + key * a.v_ss + v_slot<NCH>(row, phys) * 8, vdst + blk * 1024);
+                lds_dma16(kp + key * src.k_ss + k_slot<NCH>(row, phys) * 8, kdst + blk * 1024);
+                lds_dma16(vp + key * src.v_ss + v_slot<NCH>(row, phys) * 8, vdst + blk * 1024);
             }
         }
         if (tl_copy < kt1 - 1) {
@@ -550,13 +596,10 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
             s[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kfrag(kt, i), qf[i >> 1], s[i & 1], 0, 0, 0);
     };
 
-    f32x16 oacc[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db) oacc[db] = f32x16{};
-
-    const float c = a.scale * kLog2e;
-    float mref = -INFINITY;
-    float lsum = 0.f;
+    mref = -INFINITY;
+    lsum = 0.f;
     f32x16 scur[2], snext[2];
     bf16x8 p[4];
     float alpha = 1.f;
@@ -767,8 +810,50 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     else
         step(t, scur, snext, F_{}, F_{});
     wait_vmcnt<0>();  // the clamped trailing copies must land before the workgroup exits
+    if (DUAL && n_pass == 2 && ps == 0) {
+        // park the first context's normalized O in LDS (bf16) and its LSE
+        const float lt1 = pair_sum(lsum);
+        lse1 = (mref + __log2f(lt1)) * kLn2;
+        const float inv = 1.0f / lt1;
+        lds_char *park = (lds_char *)smem + G::LDS + threadIdx.x * 16;
+#pragma unroll
+        for (int j = 0; j < DB * 2; ++j) {  // chunk j: values 8j .. 8j+7 of (db, gq, e) order
+            bf16x8 w;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) w[e] = (__bf16)(oacc[j / 2][(j % 2) * 8 + e] * inv);
+            *(lds_bf16x8 *)(park + j * kThreads * 16) = w;
+        }
+        __syncthreads();  // every wave is done with the ring before the second pass refills it
+    }
+    }
 
-    store_row<D, OUT_F32, ACC>(a, pl, oacc, lsum, mref, b, h, qi, qrow, slot);
+    if (!DUAL || slot >= 0) {
+        store_row<D, OUT_F32, ACC>(a, pl, oacc, lsum, mref, b, h, qi, qrow, slot);
+    } else {
+        const float lt2 = pair_sum(lsum);
+        const float lse2 = (mref + __log2f(lt2)) * kLn2;
+        if (qi >= Sq) return;
+        const float inv = 1.0f / lt2;
+        const lds_char *park = (const lds_char *)smem + G::LDS + threadIdx.x * 16;
+        char *orow = static_cast<char *>(a.o) + ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * 2;
+#pragma unroll
+        for (int j = 0; j < DB * 2; ++j) {
+            const bf16x8 o1 = *(const lds_bf16x8 *)(park + j * kThreads * 16);
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                const int db = j / 2, gq = (j % 2) * 2 + half;
+                bf16x4 w;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) w[e] = (__bf16)(oacc[db][gq * 4 + e] * inv + (float)o1[half * 4 + e]);
+                *reinterpret_cast<bf16x4 *>(orow + (db * 32 + gq * 8 + hi * 4) * 2) = w;
+            }
+        }
+        if (hi == 0) {
+            const int64_t li = ((int64_t)b * a.H + h) * a.Sq + qi;
+            if (a.lse != nullptr) a.lse[li] = lse1;
+            if (a.lse2 != nullptr) a.lse2[li] = lse2;
+        }
+    }
 }
 
 // Ping-pong schedule of the same computation (launches with many key tiles).
@@ -1222,37 +1307,56 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(AttnArgs a, AttnPlan p
     const int h = bh % a.H, b = bh / a.H;
     const int qi = qt * BM + r;
     if (qi >= a.Sq) return;
-    const int64_t u0 = (int64_t)j * pl.seg;
-    float m = -INFINITY, s = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int c0 = 0; c0 < pl.seg; c0 += FB) {
-        float l[FB];
-        f32x4 o[FB];
+    // LSE merge of n units from u0 on: (max m, sum s, weighted O acc)
+    auto merge_units = [&](int64_t u0, int n, float &m, float &s, f32x4 &acc) {
+        m = -INFINITY;
+        s = 0.f;
+        acc = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int c0 = 0; c0 < n; c0 += FB) {
+            float l[FB];
+            f32x4 o[FB];
 #pragma unroll
-        for (int k = 0; k < FB; ++k) {
-            const int64_t u = u0 + min(c0 + k, pl.seg - 1);
-            l[k] = c0 + k < pl.seg ? pl.ws_lse[u * BM + r] : -INFINITY;
-            o[k] = *reinterpret_cast<const f32x4 *>(pl.ws_o + (u * BM + r) * a.D + d);
+            for (int k = 0; k < FB; ++k) {
+                const int64_t u = u0 + min(c0 + k, n - 1);
+                l[k] = c0 + k < n ? pl.ws_lse[u * BM + r] : -INFINITY;
+                o[k] = *reinterpret_cast<const f32x4 *>(pl.ws_o + (u * BM + r) * a.D + d);
+            }
+            float mb = m;
+#pragma unroll
+            for (int k = 0; k < FB; ++k) mb = fmaxf(mb, l[k]);
+            // every key range holds at least one key, so mb is finite from the
+            // first batch on
+            const float sc = expf(m - mb);
+            s *= sc;
+            acc *= sc;
+#pragma unroll
+            for (int k = 0; k < FB; ++k) {
+                const float w = expf(l[k] - mb);
+                s += w;
+                acc += w * o[k];
+            }
+            m = mb;
         }
-        float mb = m;
-#pragma unroll
-        for (int k = 0; k < FB; ++k) mb = fmaxf(mb, l[k]);
-        // every key range holds at least one key, so mb is finite from the
-        // first batch on
-        const float sc = expf(m - mb);
-        s *= sc;
-        acc *= sc;
-#pragma unroll
-        for (int k = 0; k < FB; ++k) {
-            const float w = expf(l[k] - mb);
-            s += w;
-            acc += w * o[k];
-        }
-        m = mb;
-    }
+    };
+    const int64_t u0 = (int64_t)j * (pl.seg + pl.seg2);
+    float m, s;
+    f32x4 acc;
+    merge_units(u0, pl.seg, m, s, acc);
     const float L = m + logf(s);
     char *orow = static_cast<char *>(a.o) +
                  ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
+    const int64_t li = ((int64_t)b * a.H + h) * a.Sq + qi;
+    if (pl.seg2 > 0) {  // dual context: the second context's units, merged alike; the two results summed
+        float m2, s2;
+        f32x4 acc2;
+        merge_units(u0 + pl.seg, pl.seg2, m2, s2, acc2);
+        put_out4<OUT_F32>(orow, RunMerge{1.f, 1.0f / s, L, true}, d, acc, acc2 * (1.0f / s2));
+        if (d == 0) {
+            if (a.lse != nullptr) a.lse[li] = L;
+            if (a.lse2 != nullptr) a.lse2[li] = m2 + logf(s2);
+        }
+        return;
+    }
     RunMerge w{0.f, 1.f, L, false};
     f32x4 run[1] = {};
     if (a.run_lse != nullptr) w = run_merge(load_run(a, b, h, qi, d, 0, run), L);
@@ -1291,6 +1395,48 @@ AttnPlan make_plan(int n_qtiles, int n_tiles, int n_kt, int n_cu, int D)
             best = cost;
             pl.n_dp = rounds * n_cu;
             pl.seg = seg;
+            pl.n_units = (int)units;
+        }
+    }
+    return pl;
+}
+
+// Plan of a dual-context launch (key tiles n_kt of the first context, n_kt2
+// of the second): whole tiles run both passes (cost n_kt + n_kt2 + 2); a
+// split tile becomes seg ranges of the first context and seg2 of the second,
+// seg : seg2 close to n_kt : n_kt2, with the same cost model as above.
+AttnPlan make_plan_dual(int n_qtiles, int n_tiles, int n_kt, int n_kt2, int n_cu, int D)
+{
+    constexpr int BM = kWaves * 32;
+    AttnPlan pl{};
+    pl.n_qtiles = n_qtiles;
+    pl.n_tiles = n_tiles;
+    pl.n_kt = n_kt;
+    pl.n_kt2 = n_kt2;
+    pl.n_dp = n_tiles;
+    pl.seg = 1;
+    pl.seg2 = 1;
+    pl.n_units = 0;
+    const double whole = n_kt + n_kt2 + 2.0;
+    double best = (double)((n_tiles + n_cu - 1) / n_cu) * whole;
+    const int rounds = n_tiles / n_cu;
+    const int rem = n_tiles - rounds * n_cu;
+    if (rem == 0) return pl;
+    for (int tot = 2; tot <= n_kt + n_kt2 && tot <= 256; ++tot) {
+        const int s1 = min(max((int)lround((double)tot * n_kt / (n_kt + n_kt2)), 1), min(n_kt, tot - 1));
+        const int s2 = tot - s1;
+        if (s2 < 1 || s2 > n_kt2) continue;
+        const int64_t units = (int64_t)rem * tot;
+        if (units > 0x7fffffff - (int64_t)n_tiles) break;
+        const int64_t sk_rounds = (units + n_cu - 1) / n_cu;
+        const int len = max((n_kt + s1 - 1) / s1, (n_kt2 + s2 - 1) / s2);
+        const double traffic = 2.0 * units * BM * (D + 1) * 4 / 5e12 / 1e-6;
+        const double cost = rounds * whole + sk_rounds * (len + 1.5) + traffic;
+        if (cost < best) {
+            best = cost;
+            pl.n_dp = rounds * n_cu;
+            pl.seg = s1;
+            pl.seg2 = s2;
             pl.n_units = (int)units;
         }
     }
@@ -1349,7 +1495,9 @@ hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream)
 {
     constexpr int BM = kWaves * 32;
     AttnPlan pl{};
-    if (!plan_attn(a.B, a.H, a.Sq, a.Skv, D, cu_count(), &pl)) return hipErrorInvalidConfiguration;
+    if (OUT_F32 && a.k2 != nullptr) return hipErrorInvalidValue;  // dual context: bf16 output only
+    if (!plan_attn(a.B, a.H, a.Sq, a.Skv, D, cu_count(), &pl, a.k2 != nullptr ? a.Skv2 : 0))
+        return hipErrorInvalidConfiguration;
     void *ws = nullptr;
     if (pl.n_units > 0) {
         const size_t bytes = workspace_bytes(pl, D);
@@ -1362,7 +1510,10 @@ hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream)
     const dim3 grid((unsigned)(pl.n_dp + pl.n_units)), block(kThreads);
     const int forced = forced_schedule();
     const bool pp = forced == 1 || (forced == 0 && pl.n_kt >= kPingPongMinTiles);
-    if (a.run_lse != nullptr) {
+    if (a.k2 != nullptr) {
+        if constexpr (!OUT_F32)
+            hipLaunchKernelGGL((attn_fwd_kernel<D, false, false, true>), grid, block, 0, stream, a, pl);
+    } else if (a.run_lse != nullptr) {
         if (pp)
             hipLaunchKernelGGL((attn_fwd_pingpong_kernel<D, OUT_F32, true>), grid, block, 0, stream, a, pl);
         else
@@ -1388,7 +1539,7 @@ hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream)
 
 }  // namespace
 
-bool plan_attn(int B, int H, int Sq, int Skv, int D, int n_cu, AttnPlan *out)
+bool plan_attn(int B, int H, int Sq, int Skv, int D, int n_cu, AttnPlan *out, int Skv2)
 {
     constexpr int BM = kWaves * 32;
     if (B < 0 || H < 0 || Sq < 0 || Skv < 1 || n_cu < 1) return false;
@@ -1397,7 +1548,12 @@ bool plan_attn(int B, int H, int Sq, int Skv, int D, int n_cu, AttnPlan *out)
     if (per_batch > 0x7fffffff || (B > 0 && per_batch > 0x7fffffff / B)) return false;
     const int64_t n_tiles = per_batch * B;
     const int n_kt = (int)(((int64_t)Skv + kBlockN - 1) / kBlockN);
-    *out = make_plan((int)n_qtiles, (int)n_tiles, n_kt, n_cu, D);
+    if (Skv2 < 0) return false;
+    if (Skv2 > 0)
+        *out = make_plan_dual((int)n_qtiles, (int)n_tiles, n_kt, (int)(((int64_t)Skv2 + kBlockN - 1) / kBlockN), n_cu,
+                              D);
+    else
+        *out = make_plan((int)n_qtiles, (int)n_tiles, n_kt, n_cu, D);
     return true;
 }
 

@@ -30,13 +30,23 @@ struct AttnArgs {
     const float *run_o;
     float *run_lse;
     int64_t r_sb, r_ss, r_sh;
+    // Dual context (k2 set): O = softmax(s Q K^T) V + softmax(s Q K2^T) V2,
+    // the two context attentions summed with Q read once; lse gets the first
+    // context's LSE and lse2 (may be null) the second's.  bf16 O only.
+    const void *k2, *v2;
+    float *lse2;
+    int64_t k2_sb, k2_ss, k2_sh;
+    int64_t v2_sb, v2_ss, v2_sh;
+    int32_t Skv2;
+    bool kv2_off32;
 };
 
 // Work plan of one attention launch.  Query tiles [0, n_dp) are processed
 // whole, one workgroup each (data-parallel rounds); tiles [n_dp, n_tiles) are
 // each split into `seg` contiguous key ranges ("units", one workgroup each)
 // whose normalized partial O and LSE go to a workspace and are combined by a
-// log-sum-exp fixup.  Splitting only the leftover tiles keeps every CU busy
+// log-sum-exp fixup (in dual launches: seg ranges over the first context,
+// then seg2 over the second, each context merged by LSE and the two summed).  Splitting only the leftover tiles keeps every CU busy
 // when the tile count is just above a multiple of the CU count.  The units
 // are the first n_units workgroups of the grid, the whole tiles follow.
 struct AttnPlan {
@@ -45,7 +55,9 @@ struct AttnPlan {
     int32_t n_kt;      // key tiles per query tile
     int32_t n_dp;      // tiles processed whole
     int32_t seg;       // key ranges per split tile (>= 2 when n_units > 0)
-    int32_t n_units;   // (n_tiles - n_dp) * seg
+    int32_t n_units;   // (n_tiles - n_dp) * (seg + seg2)
+    int32_t n_kt2;     // key tiles of the second context (dual launches; else 0)
+    int32_t seg2;      // key ranges of a split tile over the second context (else 0)
     float *ws_o;       // [n_units][query tile rows][D] partial O (normalized)
     float *ws_lse;     // [n_units][query tile rows] partial LSE
 };
@@ -85,7 +97,7 @@ struct NormRopeArgs {
 
 // Work plan of an attention launch of this shape on n_cu compute units
 // (host-only); false if the shape has no valid plan (Skv < 1, too many tiles).
-bool plan_attn(int B, int H, int Sq, int Skv, int D, int n_cu, AttnPlan *out);
+bool plan_attn(int B, int H, int Sq, int Skv, int D, int n_cu, AttnPlan *out, int Skv2 = 0);
 // Bytes of split-tile partials a plan needs (0 when nothing is split).
 size_t workspace_bytes(const AttnPlan &pl, int D);
 

@@ -210,3 +210,37 @@ def test_ring_accumulate_in_place_and_separate_output_pass_validation(lib):
     expect(lib, ring(lib), _lib.ERR_HIP, "hip")
     expect(lib, ring(lib, out=T(FAKE + 0x3000000), dtype=_lib.F32), _lib.ERR_HIP, "hip")
     expect(lib, ring(lib, out=T(FAKE + 0x5000000), dtype=_lib.BF16), _lib.ERR_HIP, "hip")
+
+
+def dual(lib, q=None, kt=None, vt=None, ki=None, vi=None, o=None, lt=None, li=None, St=64, Si=33, B=1, H=2, Sq=64,
+         D=128, scale=0.088):
+    q = q if q is not None else T(FAKE, S=Sq, H=H, D=D)
+    kt = kt if kt is not None else T(FAKE + 0x1000000, S=St, H=H, D=D)
+    vt = vt if vt is not None else T(FAKE + 0x2000000, S=St, H=H, D=D)
+    ki = ki if ki is not None else T(FAKE + 0x7000000, S=Si, H=H, D=D)
+    vi = vi if vi is not None else T(FAKE + 0x8000000, S=Si, H=H, D=D)
+    o = o if o is not None else T(FAKE + 0x3000000, S=Sq, H=H, D=D)
+    byref = lambda t: ctypes.byref(t) if t is not False else None  # noqa: E731
+    return lib.regenvc_cross_attn_dual_fwd(byref(q), byref(kt), byref(vt), St, byref(ki), byref(vi), Si, byref(o),
+                                           lt, li, B, H, Sq, D, scale, None)
+
+
+def test_cross_attn_dual_validation(lib):
+    expect(lib, dual(lib, ki=False), _lib.ERR_INVALID_ARG, "NULL")
+    expect(lib, dual(lib, Si=0), _lib.ERR_INVALID_ARG, "second context")
+    expect(lib, dual(lib, St=0), _lib.ERR_INVALID_ARG, "key count")
+    expect(lib, dual(lib, D=96), _lib.ERR_UNSUPPORTED, "head dim")
+    expect(lib, dual(lib, vi=T(FAKE + 0x8000000, ss=100)), _lib.ERR_UNSUPPORTED, "multiple of 8")
+    expect(lib, dual(lib, ki=T(FAKE + 0x7000008)), _lib.ERR_UNSUPPORTED, "aligned")
+    expect(lib, dual(lib, o=T(FAKE + 0x7000000)), _lib.ERR_INVALID_ARG, "overlaps")        # o on k_img
+    expect(lib, dual(lib, li=FAKE + 0x4000002), _lib.ERR_UNSUPPORTED, "aligned")
+    expect(lib, dual(lib, li=FAKE + 0x8000000), _lib.ERR_INVALID_ARG, "lse_img overlaps")  # on v_img
+    expect(lib, dual(lib, lt=FAKE + 0x4000000, li=FAKE + 0x4000000 + 64), _lib.ERR_INVALID_ARG, "lse_img overlaps")
+    expect(lib, dual(lib, lt=FAKE + 0x7000000), _lib.ERR_INVALID_ARG, "lse overlaps")      # lse_txt on k_img
+    expect(lib, dual(lib, B=0), _lib.OK)
+    expect(lib, dual(lib, Sq=0, ki=False), _lib.ERR_INVALID_ARG, "NULL")
+
+
+@pytest.mark.skipif(has_gpu_node(), reason="would reach a launch on fake addresses on a GPU machine")
+def test_cross_attn_dual_valid_arguments_reach_the_device_check(lib):
+    expect(lib, dual(lib, lt=FAKE + 0x4000000, li=FAKE + 0x4100000), _lib.ERR_HIP, "hip")

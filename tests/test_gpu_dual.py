@@ -1,0 +1,123 @@
+"""GPU parity of the dual cross-attention (regenvc_cross_attn_dual_fwd):
+text and image context attentions summed, Q read once, against the oracle's
+definition (two fp64 attentions added) on the same seeded bf16 inputs.
+
+Tolerance: max |dO| <= 1e-2 and <= 1e-2 * max|O| as for the single-context
+calls, LSE of each context <= 1e-3.  The kernel holds the text result in
+bf16 between its two passes, which adds at most 2^-9 * max|O_txt| (the
+rounding of one bf16 output) -- far below the bar at the configurations'
+|O| < 1.  Degenerate contexts of one or a few keys return a value row
+itself, |O| up to ~4, where the bf16 rounding of the output alone reaches
+2^-9 * |O| ~ 8e-3: there the bar is max(1e-2, 2^-8 * max|O|), the two
+roundings' bound."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_28144_amd import synth
+from test_gpu_parity import api, assert_close, dev, dev_head_major, host, sample_rows
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    yield
+    torch.cuda.synchronize()
+
+
+def _inputs(seed, B, H, Sq, St, Si, D):
+    rng = np.random.default_rng(seed)
+    q = synth.normal_bf16(rng, (B, Sq, H, D))
+    kt, vt = synth.normal_bf16(rng, (B, St, H, D)), synth.normal_bf16(rng, (B, St, H, D))
+    ki, vi = synth.normal_bf16(rng, (B, Si, H, D)), synth.normal_bf16(rng, (B, Si, H, D))
+    return q, kt, vt, ki, vi
+
+
+def _check(name, q, kt, vt, ki, vi, rows=None, layout="bshd", heads=None):
+    D = q.shape[3]
+    scale = synth.default_scale(D)
+    to = dev if layout == "bshd" else dev_head_major
+    o, lt, li = api().cross_attn_dual_fwd(to(q), to(kt), to(vt), to(ki), to(vi), scale=scale)
+    torch.cuda.synchronize()
+    og, ltg, lig = host(o), lt.cpu().numpy(), li.cpu().numpy()
+    if heads is not None:
+        sl = slice(heads[0], heads[1])
+        q, kt, vt, ki, vi = (np.ascontiguousarray(x[:, :, sl]) for x in (q, kt, vt, ki, vi))
+        og, ltg, lig = og[:, :, sl], ltg[:, sl], lig[:, sl]
+    if rows is not None:
+        q = np.ascontiguousarray(q[:, rows])
+        og, ltg, lig = og[:, rows], ltg[:, :, rows], lig[:, :, rows]
+    o_ref, lt_ref, li_ref = oracle.cross_attn_dual(q, kt, vt, ki, vi, scale)
+    assert_close(name + " (O, text LSE)", og, o_ref, ltg, lt_ref,
+                 o_tol=max(1e-2, 2.0 ** -8 * float(np.abs(o_ref).max())))
+    err = float(np.abs(lig - li_ref).max())
+    print(f"[parity] {name}: image max|dLSE|={err:.3e}", flush=True)
+    assert err <= 1e-3
+    return o, lt, li
+
+
+def test_window_to_text_and_image_contexts():
+    """10920 video tokens (7 x 30 x 52), 12 heads, 512 text + 257 image
+    tokens: sampled rows of every head."""
+    q, kt, vt, ki, vi = _inputs(60, 1, 12, 10920, 512, 257, 128)
+    _check("dual window", q, kt, vt, ki, vi, rows=sample_rows(10920, 200, 60))
+
+
+def test_window_split_tiles_all_rows():
+    """The window's 516 query tiles exceed two rounds of 256 CUs by four: the
+    last four (head 11, queries 9984..10919) are split into key ranges of
+    each context and recombined by the fixup.  Every one of their rows."""
+    q, kt, vt, ki, vi = _inputs(61, 1, 12, 10920, 512, 257, 128)
+    _check("dual window split tiles", q, kt, vt, ki, vi, rows=np.arange(9984 - 64, 10920), heads=(11, 12))
+
+
+@pytest.mark.parametrize("B,H,Sq,St,Si,D", [
+    (2, 2, 300, 77, 1, 128),      # single-token image context, ragged text context
+    (1, 3, 257, 64, 65, 64),      # D=64, ragged query tile
+    (1, 1, 1, 1, 1, 128),         # one query, one key each
+    (2, 3, 700, 512, 257, 128),   # the paper's context lengths, several query tiles per head
+])
+def test_ragged_shapes(B, H, Sq, St, Si, D):
+    _check(f"dual B={B} H={H} Sq={Sq} St={St} Si={Si} D={D}", *_inputs(62 + Sq, B, H, Sq, St, Si, D))
+
+
+def test_head_major_layout_matches_token_major_bitwise():
+    x = _inputs(63, 1, 4, 500, 512, 257, 128)
+    scale = synth.default_scale(128)
+    o1, l1, m1 = api().cross_attn_dual_fwd(*(dev(t) for t in x), scale=scale)
+    o2, l2, m2 = api().cross_attn_dual_fwd(*(dev_head_major(t) for t in x), scale=scale)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2) and torch.equal(m1, m2)
+
+
+def test_equals_the_two_single_context_calls_summed():
+    """Against the library's own single-context calls (f32 outputs, summed):
+    the only difference is the bf16 parking of the text result and the final
+    rounding, so |dO| <= 2^-8 * max|O|."""
+    x = _inputs(64, 1, 12, 3000, 512, 257, 128)
+    scale = synth.default_scale(128)
+    q, kt, vt, ki, vi = (dev(t) for t in x)
+    o, lt, li = api().cross_attn_dual_fwd(q, kt, vt, ki, vi, scale=scale)
+    ot, ltt = api().cross_attn_fwd(q, kt, vt, scale=scale, out_dtype=torch.float32)
+    oi, lii = api().cross_attn_fwd(q, ki, vi, scale=scale, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    s = ot + oi
+    d = (o.float() - s).abs().max().item()
+    print(f"[parity] dual vs two calls summed: max|dO|={d:.3e} (max|O|={s.abs().max().item():.3e})", flush=True)
+    assert d <= 2 ** -8 * s.abs().max().item()
+    assert (lt - ltt).abs().max().item() <= 1e-5 and (li - lii).abs().max().item() <= 1e-5
+
+
+def test_without_lse_outputs():
+    x = _inputs(65, 1, 2, 300, 100, 50, 128)
+    scale = synth.default_scale(128)
+    o, lt, li = api().cross_attn_dual_fwd(*(dev(t) for t in x), scale=scale, return_lse=False)
+    torch.cuda.synchronize()
+    assert lt is None and li is None
+    o_ref, _, _ = oracle.cross_attn_dual(*x, scale)
+    assert_close("dual without LSE", o, o_ref)

@@ -293,6 +293,44 @@ def test_ring_step_from_no_keys_is_the_chunk_result_and_ignores_the_running_outp
     assert np.array_equal(orr, o) and np.array_equal(lr, lse)
 
 
+# ---------------------------------------------------------------- dual cross-attention
+def test_dual_cross_attention_matches_two_brute_force_attentions_summed():
+    rng = np.random.default_rng(22)
+    q = ints_bf16(rng, (1, 4, 2, 4), -3, 3)
+    kt, vt = ints_bf16(rng, (1, 5, 2, 4), -3, 3), ints_bf16(rng, (1, 5, 2, 4), -3, 3)
+    ki, vi = ints_bf16(rng, (1, 3, 2, 4), -3, 3), ints_bf16(rng, (1, 3, 2, 4), -3, 3)
+    scale = F32(0.5)
+    o, lt, li = oracle.cross_attn_dual(q, kt, vt, ki, vi, scale)
+    ot, ltb = brute.attn(q, kt, vt, float(scale))
+    oi, lib = brute.attn(q, ki, vi, float(scale))
+    np.testing.assert_allclose(o, np.array(ot) + np.array(oi), rtol=0, atol=1e-13)
+    np.testing.assert_allclose(lt, np.array(ltb), rtol=0, atol=1e-13)
+    np.testing.assert_allclose(li, np.array(lib), rtol=0, atol=1e-13)
+
+
+def test_dual_cross_attention_zero_queries_give_the_two_value_means():
+    """q = 0: every score is 0, each softmax is uniform over its own context:
+    O = mean(V_txt) + mean(V_img), LSE = log of each context's length."""
+    rng = np.random.default_rng(23)
+    q = np.zeros((1, 3, 2, 8), dtype=np.uint16)
+    kt, vt = synth.normal_bf16(rng, (1, 12, 2, 8)), synth.normal_bf16(rng, (1, 12, 2, 8))
+    ki, vi = synth.normal_bf16(rng, (1, 5, 2, 8)), synth.normal_bf16(rng, (1, 5, 2, 8))
+    o, lt, li = oracle.cross_attn_dual(q, kt, vt, ki, vi, F32(0.7))
+    want = widen(vt).mean(axis=1, keepdims=True) + widen(vi).mean(axis=1, keepdims=True)
+    np.testing.assert_allclose(o, np.broadcast_to(want, o.shape), rtol=0, atol=1e-14)
+    assert np.allclose(lt, math.log(12), atol=1e-14) and np.allclose(li, math.log(5), atol=1e-14)
+
+
+def test_dual_cross_attention_is_two_softmaxes_not_one_joint_softmax():
+    """Identical contexts: the sum of two separate attentions is twice one
+    attention (a joint softmax over both would return it once)."""
+    q, k, v = synth.qkv(24, 1, 2, 6, 20, 8)
+    o, lt, li = oracle.cross_attn_dual(q, k, v, k, v, F32(0.4))
+    o1, l1 = oracle.attn(q, k, v, F32(0.4))
+    np.testing.assert_allclose(o, 2.0 * o1, rtol=0, atol=1e-14)
+    assert np.array_equal(lt, l1) and np.array_equal(li, l1)
+
+
 # ---------------------------------------------------------------- planted mistakes
 # Plausible slips in the oracle, planted in a copy of its source; each must
 # make at least one pin fail.
