@@ -28,7 +28,7 @@ sys.path.insert(0, REPO)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
-WINDOW = dict(B=1, H=12, S=10920, D=128, ctx=512, seed=3)
+WINDOW = dict(B=1, H=12, S=10920, D=128, ctx=512, img=257, seed=3)
 SHARE = dict(B=1, H=5, S=10920, D=128, chunks=4, seed=4)
 
 
@@ -155,12 +155,15 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=20, help="untimed steps (the clock settles under load)")
-    ap.add_argument("--only", choices=["self", "cross", "share", "ring", "copy", "normrope"], default=None,
+    ap.add_argument("--only", choices=["self", "cross", "share", "ring", "dual", "cross2", "copy", "normrope"],
+                    default=None,
                     help="time one component alone (for profiling); 'copy' runs a plain 1 GiB elementwise "
                          "copy kernel, the reference for scaling HBM byte counters; 'normrope' times the q/k "
                          "RMSNorm + 3D rotary embedding that produces the window's attention inputs (not part "
                          "of the attention step); 'ring' runs the share with the merge fused into each chunk "
-                         "(first chunk's partial, then ring-accumulate steps, the last into bf16)")
+                         "(first chunk's partial, then ring-accumulate steps, the last into bf16); 'dual' "
+                         "times the text (512) + image (257) cross-attention summed in one call, 'cross2' the "
+                         "same two contexts as two separate cross-attention calls (without the sum)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle sample")
     args = ap.parse_args()
@@ -198,6 +201,11 @@ def main():
     l_self = torch.empty((B, H, S), dtype=torch.float32, device=dev)
     o_cross = torch.empty_like(o_self)
     l_cross = torch.empty_like(l_self)
+    l_img = torch.empty_like(l_self)
+    ki = vi = None
+    if args.only in ("dual", "cross2"):
+        rng = np.random.default_rng(W["seed"] + 100)
+        ki, vi = (to_dev(synth.normal_bf16(rng, (B, W["img"], H, D))) for _ in range(2))
     nch = R["chunks"]
     csz = R["S"] // nch
     bounds = [i * csz for i in range(nch)] + [R["S"]]
@@ -212,6 +220,8 @@ def main():
         "cross": attn_flops(B, H, S, W["ctx"], D),
         "share": attn_flops(R["B"], R["H"], R["S"], R["S"], R["D"]),
         "ring": attn_flops(R["B"], R["H"], R["S"], R["S"], R["D"]),
+        "dual": attn_flops(B, H, S, W["ctx"] + W["img"], D),
+        "cross2": attn_flops(B, H, S, W["ctx"] + W["img"], D),
     }
     stream = torch.cuda.current_stream(dev)
     ev = {c: [] for c in comps}
@@ -225,6 +235,11 @@ def main():
                 api.attn_fwd(q, k, v, scale=scale, out=o_self, lse_out=l_self)
             elif c == "cross":
                 api.cross_attn_fwd(q, kc, vc, scale=scale, out=o_cross, lse_out=l_cross)
+            elif c == "dual":
+                api.cross_attn_dual_fwd(q, kc, vc, ki, vi, scale=scale, out=o_cross, lse_txt=l_cross, lse_img=l_img)
+            elif c == "cross2":
+                api.cross_attn_fwd(q, kc, vc, scale=scale, out=o_cross, lse_out=l_cross)
+                api.cross_attn_fwd(q, ki, vi, scale=scale, out=o_self, lse_out=l_img)
             elif c == "share":
                 for i in range(nch):
                     a, b = bounds[i], bounds[i + 1]
