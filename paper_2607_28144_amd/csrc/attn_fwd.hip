@@ -418,6 +418,44 @@ __device__ __forceinline__ void store_row(const AttnArgs &a, const AttnPlan &pl,
     }
 }
 
+// bf16 output of a whole tile of the interleaved kernel, as full rows: each
+// wave stages its 32 rows (this lane: row `col`, values at d = db*32 + gq*8 +
+// hi*4 + e, already final) in LDS at `stg` (32 * D * 2 bytes, 16-byte chunks
+// XOR-swizzled by row), then every store instruction writes 64 / (D/8) whole
+// rows of 16-byte chunks.  Writing straight from the accumulator layout
+// instead scatters each instruction over 32 rows, 16 bytes apiece, and the
+// stores of a 256-row tile then take about 60 % longer to drain.  The caller
+// has made sure that no wave still reads the LDS at `stg`.
+template <int D>
+__device__ __forceinline__ void store_tile_bf16(const AttnArgs &a, lds_char *stg, const f32x16 (&val)[D / 32], int lane,
+                                                int b, int h, int row0)
+{
+    constexpr int DB = D / 32;
+    constexpr int CPR = D / 8;     // 16-byte chunks per row
+    constexpr int RPI = 64 / CPR;  // rows per store instruction
+    const int col = lane & 31, hi = lane >> 5;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq) {
+            bf16x4 w;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) w[e] = (__bf16)val[db][gq * 4 + e];
+            const int ch = (db * 4 + gq) ^ (col & (CPR - 1));
+            *(lds_bf16x4 *)(stg + col * D * 2 + ch * 16 + hi * 8) = w;
+        }
+    // the wave reads back only what it wrote: its own LDS order suffices
+#pragma unroll
+    for (int it = 0; it < 32 / RPI; ++it) {
+        const int r = it * RPI + lane / CPR, c = lane % CPR;
+        const bf16x8 w = *(const lds_bf16x8 *)(stg + r * D * 2 + (c ^ (r & (CPR - 1))) * 16);
+        const int qr = row0 + r;
+        if (qr < a.Sq)
+            *reinterpret_cast<bf16x8 *>(static_cast<char *>(a.o) +
+                                        ((int64_t)b * a.o_sb + (int64_t)qr * a.o_ss + (int64_t)h * a.o_sh) * 2 + c * 16) = w;
+    }
+}
+
 template <int N>
 __device__ __forceinline__ void wait_vmcnt()
 {
@@ -827,13 +865,23 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     }
     }
 
-    if (!DUAL || slot >= 0) {
+    if (slot >= 0 || OUT_F32 || ACC) {
         store_row<D, OUT_F32, ACC>(a, pl, oacc, lsum, mref, b, h, qi, qrow, slot);
-    } else {
-        const float lt2 = pair_sum(lsum);
-        const float lse2 = (mref + __log2f(lt2)) * kLn2;
+        return;
+    }
+    // whole tile, bf16 output: final values in oacc, then full-row stores
+    const float lt = pair_sum(lsum);
+    const float inv = 1.0f / lt;
+    const float lse_last = (mref + __log2f(lt)) * kLn2;
+    if constexpr (DUAL) {
+        // the sum goes out straight from the accumulator layout (measured
+        // faster here than staging it for full-row stores)
+        if (hi == 0 && qi < Sq) {
+            const int64_t li = ((int64_t)b * a.H + h) * a.Sq + qi;
+            if (a.lse != nullptr) a.lse[li] = lse1;
+            if (a.lse2 != nullptr) a.lse2[li] = lse_last;
+        }
         if (qi >= Sq) return;
-        const float inv = 1.0f / lt2;
         const lds_char *park = (const lds_char *)smem + G::LDS + threadIdx.x * 16;
         char *orow = static_cast<char *>(a.o) + ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * 2;
 #pragma unroll
@@ -848,12 +896,14 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
                 *reinterpret_cast<bf16x4 *>(orow + (db * 32 + gq * 8 + hi * 4) * 2) = w;
             }
         }
-        if (hi == 0) {
-            const int64_t li = ((int64_t)b * a.H + h) * a.Sq + qi;
-            if (a.lse != nullptr) a.lse[li] = lse1;
-            if (a.lse2 != nullptr) a.lse2[li] = lse2;
-        }
+        return;
+    } else {
+#pragma unroll
+        for (int db = 0; db < DB; ++db) oacc[db] *= inv;
     }
+    if (a.lse != nullptr && hi == 0 && qi < Sq) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = lse_last;
+    __syncthreads();  // every wave is done with the ring, which now stages the output
+    store_tile_bf16<D>(a, (lds_char *)smem + wave * 32 * D * 2, oacc, lane, b, h, qt * BM + wave * 32);
 }
 
 // Ping-pong schedule of the same computation (launches with many key tiles).
