@@ -418,33 +418,27 @@ __device__ __forceinline__ void store_row(const AttnArgs &a, const AttnPlan &pl,
     }
 }
 
-// bf16 output of a whole tile of the interleaved kernel, as full rows: each
-// wave stages its 32 rows (this lane: row `col`, values at d = db*32 + gq*8 +
-// hi*4 + e, already final) in LDS at `stg` (32 * D * 2 bytes, 16-byte chunks
-// XOR-swizzled by row), then every store instruction writes 64 / (D/8) whole
-// rows of 16-byte chunks.  Writing straight from the accumulator layout
-// instead scatters each instruction over 32 rows, 16 bytes apiece, and the
-// stores of a 256-row tile then take about 60 % longer to drain.  The caller
-// has made sure that no wave still reads the LDS at `stg`.
+// bf16 output of a whole tile as full rows: each wave stages its 32 rows in
+// LDS at `stg` (32 * D * 2 bytes, 16-byte chunks XOR-swizzled by row) with
+// stage_out4, then store_staged_rows writes 64 / (D/8) whole rows of 16-byte
+// chunks per store instruction.  Writing straight from the accumulator
+// layouts instead scatters each instruction over 16 or 32 rows, a few bytes
+// apiece, and the stores of a 256-row tile then take about 60 % longer to
+// drain.  The caller has made sure that no wave still reads the LDS at `stg`;
+// a wave reads back only what it wrote, so its own LDS ordering suffices.
 template <int D>
-__device__ __forceinline__ void store_tile_bf16(const AttnArgs &a, lds_char *stg, const f32x16 (&val)[D / 32], int lane,
-                                                int b, int h, int row0)
+__device__ __forceinline__ void stage_out4(lds_char *stg, int r, int d, const bf16x4 &w)
 {
-    constexpr int DB = D / 32;
+    constexpr int CPR = D / 8;  // 16-byte chunks per row
+    *(lds_bf16x4 *)(stg + r * D * 2 + (((d >> 3) ^ (r & (CPR - 1))) << 4) + (d & 4) * 2) = w;
+}
+
+template <int D>
+__device__ __forceinline__ void store_staged_rows(const AttnArgs &a, const lds_char *stg, int lane, int b, int h,
+                                                  int row0)
+{
     constexpr int CPR = D / 8;     // 16-byte chunks per row
     constexpr int RPI = 64 / CPR;  // rows per store instruction
-    const int col = lane & 31, hi = lane >> 5;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int gq = 0; gq < 4; ++gq) {
-            bf16x4 w;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) w[e] = (__bf16)val[db][gq * 4 + e];
-            const int ch = (db * 4 + gq) ^ (col & (CPR - 1));
-            *(lds_bf16x4 *)(stg + col * D * 2 + ch * 16 + hi * 8) = w;
-        }
-    // the wave reads back only what it wrote: its own LDS order suffices
 #pragma unroll
     for (int it = 0; it < 32 / RPI; ++it) {
         const int r = it * RPI + lane / CPR, c = lane % CPR;
@@ -454,6 +448,26 @@ __device__ __forceinline__ void store_tile_bf16(const AttnArgs &a, lds_char *stg
             *reinterpret_cast<bf16x8 *>(static_cast<char *>(a.o) +
                                         ((int64_t)b * a.o_sb + (int64_t)qr * a.o_ss + (int64_t)h * a.o_sh) * 2 + c * 16) = w;
     }
+}
+
+// Interleaved layout: this lane holds row `col` (lane % 32), values at
+// d = db*32 + gq*8 + hi*4 + e, already final.
+template <int D>
+__device__ __forceinline__ void store_tile_bf16(const AttnArgs &a, lds_char *stg, const f32x16 (&val)[D / 32], int lane,
+                                                int b, int h, int row0)
+{
+    constexpr int DB = D / 32;
+    const int col = lane & 31, hi = lane >> 5;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq) {
+            bf16x4 w;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) w[e] = (__bf16)val[db][gq * 4 + e];
+            stage_out4<D>(stg, col, db * 32 + gq * 8 + hi * 4, w);
+        }
+    store_staged_rows<D>(a, stg, lane, b, h, row0);
 }
 
 template <int N>
@@ -1293,6 +1307,33 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     // Epilogue: per query, l = the sum of the four lanes' partial sums;
     // O = O^T / l, LSE = ln2 * (m_ref + log2 l); a split tile's key range
     // writes its normalized partial to the workspace instead.
+    if constexpr (!OUT_F32 && !ACC) {
+        if (slot < 0) {  // whole tile, bf16: staged full-row stores
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb) {
+                const float lt = quad_sum(lsum[qb]);
+                const float inv = 1.0f / lt;
+                const int qi = qi0 + qb * 16;
+                if (a.lse != nullptr && g == 0 && qi < a.Sq)
+                    a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = (mref[qb] + __log2f(lt)) * kLn2;
+#pragma unroll
+                for (int db = 0; db < DB; ++db) oacc[db][qb] *= inv;
+            }
+            __syncthreads();  // every wave is done with the ring, which now stages the output
+            lds_char *stg = (lds_char *)smem + wave * 32 * D * 2;
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    bf16x4 w;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) w[e] = (__bf16)oacc[db][qb][e];
+                    stage_out4<D>(stg, qb * 16 + x, db * 16 + g * 4, w);
+                }
+            store_staged_rows<D>(a, stg, lane, b, h, qt * BM + wave * 32);
+            return;
+        }
+    }
     // In the ring-accumulate mode the running state of both rows is loaded
     // first, in one batch.
     f32x4 run[2][ACC ? DB : 1] = {};
