@@ -450,6 +450,31 @@ __device__ __forceinline__ void store_staged_rows(const AttnArgs &a, const lds_c
     }
 }
 
+// The same for f32 rows (32 * D * 4 bytes of LDS per wave).
+template <int D>
+__device__ __forceinline__ void stage_out4_f32(lds_char *stg, int r, int d, const f32x4 &w)
+{
+    constexpr int CPR = D / 4;  // 16-byte chunks per row
+    *(__attribute__((address_space(3))) f32x4 *)(stg + r * D * 4 + (((d >> 2) ^ (r & (CPR - 1))) << 4)) = w;
+}
+
+template <int D>
+__device__ __forceinline__ void store_staged_rows_f32(const AttnArgs &a, const lds_char *stg, int lane, int b, int h,
+                                                      int row0)
+{
+    constexpr int CPR = D / 4;     // 16-byte chunks per row
+    constexpr int RPI = 64 / CPR;  // rows per store instruction
+#pragma unroll
+    for (int it = 0; it < 32 / RPI; ++it) {
+        const int r = it * RPI + lane / CPR, c = lane % CPR;
+        const f32x4 w = *(const __attribute__((address_space(3))) f32x4 *)(stg + r * D * 4 + (c ^ (r & (CPR - 1))) * 16);
+        const int qr = row0 + r;
+        if (qr < a.Sq)
+            *reinterpret_cast<f32x4 *>(static_cast<char *>(a.o) +
+                                       ((int64_t)b * a.o_sb + (int64_t)qr * a.o_ss + (int64_t)h * a.o_sh) * 4 + c * 16) = w;
+    }
+}
+
 // Interleaved layout: this lane holds row `col` (lane % 32), values at
 // d = db*32 + gq*8 + hi*4 + e, already final.
 template <int D>
@@ -1307,8 +1332,8 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     // Epilogue: per query, l = the sum of the four lanes' partial sums;
     // O = O^T / l, LSE = ln2 * (m_ref + log2 l); a split tile's key range
     // writes its normalized partial to the workspace instead.
-    if constexpr (!OUT_F32 && !ACC) {
-        if (slot < 0) {  // whole tile, bf16: staged full-row stores
+    if constexpr (!ACC) {
+        if (slot < 0) {  // whole tile: staged full-row stores (f32 rows take the whole 128 KB ring)
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb) {
                 const float lt = quad_sum(lsum[qb]);
@@ -1320,17 +1345,25 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
                 for (int db = 0; db < DB; ++db) oacc[db][qb] *= inv;
             }
             __syncthreads();  // every wave is done with the ring, which now stages the output
-            lds_char *stg = (lds_char *)smem + wave * 32 * D * 2;
+            lds_char *stg = (lds_char *)smem + wave * 32 * D * (OUT_F32 ? 4 : 2);
+            static_assert(!OUT_F32 || kWaves * 32 * D * 4 <= G::LDS, "f32 staging fits the ring");
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
                 for (int db = 0; db < DB; ++db) {
-                    bf16x4 w;
+                    if constexpr (OUT_F32) {
+                        stage_out4_f32<D>(stg, qb * 16 + x, db * 16 + g * 4, oacc[db][qb]);
+                    } else {
+                        bf16x4 w;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) w[e] = (__bf16)oacc[db][qb][e];
-                    stage_out4<D>(stg, qb * 16 + x, db * 16 + g * 4, w);
+                        for (int e = 0; e < 4; ++e) w[e] = (__bf16)oacc[db][qb][e];
+                        stage_out4<D>(stg, qb * 16 + x, db * 16 + g * 4, w);
+                    }
                 }
-            store_staged_rows<D>(a, stg, lane, b, h, qt * BM + wave * 32);
+            if constexpr (OUT_F32)
+                store_staged_rows_f32<D>(a, stg, lane, b, h, qt * BM + wave * 32);
+            else
+                store_staged_rows<D>(a, stg, lane, b, h, qt * BM + wave * 32);
             return;
         }
     }
