@@ -111,6 +111,12 @@ __device__ __forceinline__ int k_slot(int row, int ch) { return ch ^ (row & (NCH
 template <int NCH>
 __device__ __forceinline__ int v_slot(int row, int ch) { return ch ^ ((4 * (row & 3)) & (NCH - 1)); }
 
+// The copies below name M0 as clobbered: they set it to the LDS destination,
+// and the compiler must not keep a value of its own there across them.  Clang
+// warns that M0 is a reserved register; the clobber is still honoured (it
+// reloads M0 before its own uses), so the warning is silenced here only.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
 // 16-byte HBM -> LDS copy (global_load_lds_dwordx4): lane i's 16 bytes land at
 // lds_base + 16 * i.  Written as inline asm so the compiler does not treat it
 // as an LDS store it must wait for before every later LDS read (it cannot
@@ -164,6 +170,7 @@ __device__ __forceinline__ void lds_dma16_group(const uint16_t *base, const uint
                          : "m0");
     }
 }
+#pragma clang diagnostic pop
 
 // A pointer the caller knows to be wave-uniform, moved to scalar registers.
 __device__ __forceinline__ const uint16_t *uniform_ptr(const uint16_t *p)
