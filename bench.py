@@ -8,6 +8,9 @@ One step = one pass of the whole hot path over one synthetic batch:
   share  one sequence-parallel rank's share: H=5, Sq=10920, keys in 4
          contiguous chunks of 2730 -> 4 partials (fp32 O + LSE) -> LSE merge
          into bf16 O
+Beside the step, "extras" times the rank share through ring steps (the
+merge fused into each chunk) and the text (512) + image (257) dual
+cross-attention; they are not part of `value`.
 Inputs are resident in HBM before the timed region.  `value` is the step's
 algorithmic attention FLOPs (4*B*H*Sq*Skv*d per attention call, softmax and
 padding excluded) divided by the step time.  Prints ONE JSON line.
@@ -148,6 +151,47 @@ def normrope_bench(torch, dev, args):
                                              "(7x30x52) H=12 d=128 bf16"},
                       "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                    "frac": gbs / PEAK_HBM_GBS, "traffic": None}}), flush=True)
+
+
+def next_steps_timing(torch, api, synth, dev, to_dev, q, kc, vc, rq, rk, rv, scale, bounds, o_parts, l_parts,
+                      o_share, o_cross, l_cross, steps=20):
+    """Beside the step (not part of `value`): the rank share through ring
+    steps (the merge fused into each chunk's epilogue) and the text + image
+    dual cross-attention, each timed alone with HIP events."""
+    W = WINDOW
+    B, H, S, D = W["B"], W["H"], W["S"], W["D"]
+    rng = np.random.default_rng(W["seed"] + 100)
+    ki, vi = (to_dev(synth.normal_bf16(rng, (B, W["img"], H, D))) for _ in range(2))
+    l_img = torch.empty_like(l_cross)
+    nch = len(bounds) - 1
+
+    def ring():
+        api.attn_partial_fwd(rq, rk[:, :bounds[1]], rv[:, :bounds[1]], scale=scale, out=o_parts[0],
+                             lse_out=l_parts[0])
+        for i in range(1, nch):
+            a, b = bounds[i], bounds[i + 1]
+            api.attn_ring_accumulate(rq, rk[:, a:b], rv[:, a:b], o_parts[0], l_parts[0], scale=scale,
+                                     out=o_share if i == nch - 1 else None, out_dtype=torch.bfloat16)
+
+    def dual():
+        api.cross_attn_dual_fwd(q, kc, vc, ki, vi, scale=scale, out=o_cross, lse_txt=l_cross, lse_img=l_img)
+
+    out = {}
+    stream = torch.cuda.current_stream(dev)
+    for name, fn, gflop in [("share_ring", ring, attn_flops(1, SHARE["H"], SHARE["S"], SHARE["S"], SHARE["D"]) / 1e9),
+                            ("dual_cross_512_257", dual, attn_flops(B, H, S, W["ctx"] + W["img"], D) / 1e9)]:
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        out[name] = {"ms": ms, "gflop": gflop, "tflops": gflop / ms}
+    return out
 
 
 def main():
@@ -321,6 +365,9 @@ def main():
         "roofline": roofline,
         "cpu_baseline": None,
     }
+    if args.only is None:
+        line["extras"] = next_steps_timing(torch, api, synth, dev, to_dev, q, kc, vc, rq, rk, rv, scale, bounds,
+                                           o_parts, l_parts, o_share, o_cross, l_cross)
     if not args.no_cpu_baseline and args.only is None:
         print("[bench] timing the oracle on the host cores", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(args.cpu_seconds)

@@ -123,3 +123,21 @@ def test_ring_split_tiles_go_through_the_fixup():
     o_ref, l_ref = oracle.attn(qs, _chunk(hk, 0, 5460), _chunk(hv, 0, 5460), scale)
     assert_close("ring split tiles head 11", host(out)[:, rows][:, :, 11:12], o_ref,
                  lse_run.cpu().numpy()[:, 11:12][:, :, rows], l_ref)
+
+
+def test_ring_step_into_a_separate_f32_output_leaves_the_running_output():
+    """o_out given in f32: the merged output goes there, o_run is only read
+    (unchanged), and lse_run is updated in place."""
+    q, k, v = synth.qkv(56, 1, 2, 300, 600, 128)
+    scale = synth.default_scale(128)
+    dq, dk, dv = dev(q), dev(k), dev(v)
+    o_run, lse_run = api().attn_partial_fwd(dq, dk[:, :250], dv[:, :250], scale=scale)
+    before = o_run.clone()
+    out = torch.empty_like(o_run)
+    res = api().attn_ring_accumulate(dq, dk[:, 250:], dv[:, 250:], o_run, lse_run, scale=scale, out=out,
+                                     out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert res.data_ptr() == out.data_ptr()
+    assert torch.equal(o_run, before)
+    o_ref, l_ref = oracle.attn(q, k, v, scale)
+    assert_close("ring step into a separate f32 output", out, o_ref, lse_run, l_ref)
