@@ -482,6 +482,57 @@ __device__ __forceinline__ void store_staged_rows_f32(const AttnArgs &a, const l
     }
 }
 
+// Staged rows of the ring accumulate: the staged values are this launch's
+// normalized O times its merge weight; row r then adds w_r * O_run, with w_r
+// < 0 marking a row without running state (O_run ignored).  w_r is held by
+// lane r % 16 of the ping-pong layout, as wr[r / 16].  All O_run chunks are
+// loaded before the first store (the output may be O_run itself).
+template <int D, bool OUT_F32>
+__device__ __forceinline__ void store_staged_rows_run(const AttnArgs &a, const lds_char *stg, int lane, int b, int h,
+                                                      int row0, const float (&wr)[2])
+{
+    constexpr int ESZ = OUT_F32 ? 4 : 2;
+    constexpr int CPR = D * ESZ / 16;  // 16-byte chunks per row
+    constexpr int VPC = 16 / ESZ;      // values per chunk
+    constexpr int RPI = 64 / CPR;      // rows per instruction (divides 16)
+    constexpr int NIT = 32 / RPI;
+    static_assert(16 % RPI == 0, "one query block per instruction");
+    f32x4 run[NIT][VPC / 4];
+    float w[NIT];
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+        const int r = it * RPI + lane / CPR, c = lane % CPR;
+        w[it] = __shfl(it * RPI < 16 ? wr[0] : wr[1], r & 15, 64);
+        const int qc = min(row0 + r, a.Sq - 1);
+        const float *rrow = a.run_o + ((int64_t)b * a.r_sb + (int64_t)qc * a.r_ss + (int64_t)h * a.r_sh) + c * VPC;
+#pragma unroll
+        for (int k = 0; k < VPC / 4; ++k) run[it][k] = *reinterpret_cast<const f32x4 *>(rrow + 4 * k);
+    }
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+        const int r = it * RPI + lane / CPR, c = lane % CPR;
+        const int qr = row0 + r;
+        const lds_char *src = stg + r * D * ESZ + (c ^ (r & (CPR - 1))) * 16;
+        char *dst = static_cast<char *>(a.o) + ((int64_t)b * a.o_sb + (int64_t)qr * a.o_ss + (int64_t)h * a.o_sh) * ESZ +
+                    c * 16;
+        if constexpr (OUT_F32) {
+            f32x4 v = *(const __attribute__((address_space(3))) f32x4 *)src;
+            if (w[it] >= 0.f) v += run[it][0] * w[it];
+            if (qr < a.Sq) *reinterpret_cast<f32x4 *>(dst) = v;
+        } else {
+            const bf16x8 sv = *(const lds_bf16x8 *)src;
+            bf16x8 o;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                float v = (float)sv[e];
+                if (w[it] >= 0.f) v += run[it][e / 4][e % 4] * w[it];
+                o[e] = (__bf16)v;
+            }
+            if (qr < a.Sq) *reinterpret_cast<bf16x8 *>(dst) = o;
+        }
+    }
+}
+
 // Interleaved layout: this lane holds row `col` (lane % 32), values at
 // d = db*32 + gq*8 + hi*4 + e, already final.
 template <int D>
@@ -1339,17 +1390,25 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     // Epilogue: per query, l = the sum of the four lanes' partial sums;
     // O = O^T / l, LSE = ln2 * (m_ref + log2 l); a split tile's key range
     // writes its normalized partial to the workspace instead.
-    if constexpr (!ACC) {
+    {
         if (slot < 0) {  // whole tile: staged full-row stores (f32 rows take the whole 128 KB ring)
+            float wr[2] = {0.f, 0.f};  // ring accumulate: the running output's weight per query block
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb) {
                 const float lt = quad_sum(lsum[qb]);
-                const float inv = 1.0f / lt;
+                float sc = 1.0f / lt;
+                float lse_val = (mref[qb] + __log2f(lt)) * kLn2;
                 const int qi = qi0 + qb * 16;
-                if (a.lse != nullptr && g == 0 && qi < a.Sq)
-                    a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = (mref[qb] + __log2f(lt)) * kLn2;
+                if constexpr (ACC) {
+                    const int qc = min(qi, a.Sq - 1);
+                    const RunMerge m = run_merge(a.run_lse[((int64_t)b * a.H + h) * a.Sq + qc], lse_val);
+                    lse_val = m.lse;
+                    sc *= m.wc;
+                    wr[qb] = m.run ? m.wr : -1.f;
+                }
+                if (a.lse != nullptr && g == 0 && qi < a.Sq) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = lse_val;
 #pragma unroll
-                for (int db = 0; db < DB; ++db) oacc[db][qb] *= inv;
+                for (int db = 0; db < DB; ++db) oacc[db][qb] *= sc;
             }
             __syncthreads();  // every wave is done with the ring, which now stages the output
             lds_char *stg = (lds_char *)smem + wave * 32 * D * (OUT_F32 ? 4 : 2);
@@ -1367,51 +1426,26 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
                         stage_out4<D>(stg, qb * 16 + x, db * 16 + g * 4, w);
                     }
                 }
-            if constexpr (OUT_F32)
+            if constexpr (ACC)
+                store_staged_rows_run<D, OUT_F32>(a, stg, lane, b, h, qt * BM + wave * 32, wr);
+            else if constexpr (OUT_F32)
                 store_staged_rows_f32<D>(a, stg, lane, b, h, qt * BM + wave * 32);
             else
                 store_staged_rows<D>(a, stg, lane, b, h, qt * BM + wave * 32);
             return;
         }
     }
-    // In the ring-accumulate mode the running state of both rows is loaded
-    // first, in one batch.
-    f32x4 run[2][ACC ? DB : 1] = {};
-    float run_l[2] = {-INFINITY, -INFINITY};
-    if constexpr (ACC) {
-        if (slot < 0) {
-#pragma unroll
-            for (int qb = 0; qb < 2; ++qb) run_l[qb] = load_run(a, b, h, qi0 + qb * 16, g * 4, 16, run[qb]);
-        }
-    }
+    // A split tile's key range: its normalized partial to the workspace.
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
         const float lt = quad_sum(lsum[qb]);
         const float inv = 1.0f / lt;
-        const float lse_val = (mref[qb] + __log2f(lt)) * kLn2;
         const int qrow = qrow0 + qb * 16, qi = qi0 + qb * 16;
         if (qi >= a.Sq) continue;
-        if (slot >= 0) {
-            float *orow = pl.ws_o + ((int64_t)slot * BM + qrow) * D;
+        float *orow = pl.ws_o + ((int64_t)slot * BM + qrow) * D;
 #pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                f32x4 w;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) w[e] = oacc[db][qb][e] * inv;
-                *reinterpret_cast<f32x4 *>(orow + db * 16 + g * 4) = w;
-            }
-            if (g == 0) pl.ws_lse[(int64_t)slot * BM + qrow] = lse_val;
-        } else {
-            char *orow = static_cast<char *>(a.o) +
-                         ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
-            RunMerge w{0.f, 1.f, lse_val, false};
-            if constexpr (ACC) w = run_merge(run_l[qb], lse_val);
-            w.wc *= inv;
-#pragma unroll
-            for (int db = 0; db < DB; ++db)
-                put_out4<OUT_F32>(orow, w, db * 16 + g * 4, oacc[db][qb], run[qb][ACC ? db : 0]);
-            if (a.lse != nullptr && g == 0) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = w.lse;
-        }
+        for (int db = 0; db < DB; ++db) *reinterpret_cast<f32x4 *>(orow + db * 16 + g * 4) = oacc[db][qb] * inv;
+        if (g == 0) pl.ws_lse[(int64_t)slot * BM + qrow] = (mref[qb] + __log2f(lt)) * kLn2;
     }
 }
 
