@@ -155,14 +155,17 @@ def normrope_bench(torch, dev, args):
 
 def next_steps_timing(torch, api, synth, dev, to_dev, q, kc, vc, rq, rk, rv, scale, bounds, o_parts, l_parts,
                       o_share, o_cross, l_cross, steps=20):
-    """Beside the step (not part of `value`): the rank share through ring
-    steps (the merge fused into each chunk's epilogue) and the text + image
-    dual cross-attention, each timed alone with HIP events."""
+    """Beside the step (not part of `value`): the rank share as partials +
+    merge and through ring steps (the merge fused into each chunk's
+    epilogue), and the text + image contexts as two cross-attention calls
+    and as one dual call; timed with HIP events, the cases of a pair
+    alternating in blocks; the best block of each is reported."""
     W = WINDOW
     B, H, S, D = W["B"], W["H"], W["S"], W["D"]
     rng = np.random.default_rng(W["seed"] + 100)
     ki, vi = (to_dev(synth.normal_bf16(rng, (B, W["img"], H, D))) for _ in range(2))
     l_img = torch.empty_like(l_cross)
+    o_img = torch.empty_like(o_cross)
     nch = len(bounds) - 1
 
     def ring():
@@ -173,25 +176,40 @@ def next_steps_timing(torch, api, synth, dev, to_dev, q, kc, vc, rq, rk, rv, sca
             api.attn_ring_accumulate(rq, rk[:, a:b], rv[:, a:b], o_parts[0], l_parts[0], scale=scale,
                                      out=o_share if i == nch - 1 else None, out_dtype=torch.bfloat16)
 
+    def share():
+        for i in range(nch):
+            a, b = bounds[i], bounds[i + 1]
+            api.attn_partial_fwd(rq, rk[:, a:b], rv[:, a:b], scale=scale, out=o_parts[i], lse_out=l_parts[i])
+        api.lse_merge(o_parts, l_parts, out=o_share)
+
+    def two_calls():
+        api.cross_attn_fwd(q, kc, vc, scale=scale, out=o_cross, lse_out=l_cross)
+        api.cross_attn_fwd(q, ki, vi, scale=scale, out=o_img, lse_out=l_img)
+
     def dual():
         api.cross_attn_dual_fwd(q, kc, vc, ki, vi, scale=scale, out=o_cross, lse_txt=l_cross, lse_img=l_img)
 
-    out = {}
+    # each pair is timed alternately, in blocks, under the same conditions
+    gs = attn_flops(1, SHARE["H"], SHARE["S"], SHARE["S"], SHARE["D"]) / 1e9
+    gd = attn_flops(B, H, S, W["ctx"] + W["img"], D) / 1e9
+    cases = [("share_partials_merge", share, gs), ("share_ring", ring, gs),
+             ("cross_two_calls_512_257", two_calls, gd), ("dual_cross_512_257", dual, gd)]
+    ms = {name: [] for name, _, _ in cases}
     stream = torch.cuda.current_stream(dev)
-    for name, fn, gflop in [("share_ring", ring, attn_flops(1, SHARE["H"], SHARE["S"], SHARE["S"], SHARE["D"]) / 1e9),
-                            ("dual_cross_512_257", dual, attn_flops(B, H, S, W["ctx"] + W["img"], D) / 1e9)]:
-        for _ in range(5):
+    for _, fn, _ in cases:
+        for _ in range(3):
             fn()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(steps):
-            fn()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / steps
-        out[name] = {"ms": ms, "gflop": gflop, "tflops": gflop / ms}
-    return out
+    torch.cuda.synchronize()
+    for _ in range(4):
+        for name, fn, _ in cases:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(steps // 4):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms[name].append(e0.elapsed_time(e1) / (steps // 4))
+    return {name: {"ms": min(ms[name]), "gflop": g, "tflops": g / min(ms[name])} for name, _, g in cases}
 
 
 def main():
