@@ -11,9 +11,15 @@ One step = one pass of the whole hot path over one synthetic batch:
 Beside the step, "extras" times the rank share through ring steps (the
 merge fused into each chunk) and the text (512) + image (257) dual
 cross-attention; they are not part of `value`.
-Inputs are resident in HBM before the timed region.  `value` is the step's
-algorithmic attention FLOPs (4*B*H*Sq*Skv*d per attention call, softmax and
-padding excluded) divided by the step time.  Prints ONE JSON line.
+Inputs are resident in HBM before the timed region.  `value` is the metric's
+own workload: the window self-attention's algorithmic FLOPs (4*B*H*Sq*Skv*d,
+softmax and padding excluded) divided by the average duration of that call,
+taken with HIP events on the launch stream over the timed steps (the same
+figure as roofline.achieved); the whole step's blended rate is the `step`
+component.  After the timed steps, `legs` time the other configurations
+alone: image-scale self-attention (B=1, H=12, S=4096) and the paper's own
+rank share (H=3, Sq=5460, keys in 2 chunks of 5460, partials + merge), each
+with its roofline fraction.  Prints ONE JSON line.
 """
 import argparse
 import json
@@ -33,6 +39,8 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 WINDOW = dict(B=1, H=12, S=10920, D=128, ctx=512, img=257, seed=3)
 SHARE = dict(B=1, H=5, S=10920, D=128, chunks=4, seed=4)
+IMAGE = dict(B=1, H=12, S=4096, D=128, seed=2)
+PAPER_SHARE = dict(B=1, H=3, S=10920, Sq=5460, D=128, chunks=2, seed=5)
 
 
 def measured_traffic():
@@ -64,33 +72,113 @@ def cpu_model():
     return platform.processor()
 
 
-def cpu_baseline(target_s: float):
-    """Times the fp64 oracle on a bounded sample of the window self-attention:
-    a few query rows of all 12 heads against all 10920 keys."""
-    import oracle
-    from paper_2607_28144_amd import synth
-    W = WINDOW
-    q, k, v = synth.qkv(W["seed"], W["B"], W["H"], W["S"], W["S"], W["D"])
-    scale = synth.default_scale(W["D"])
+def oracle_sample(oracle, q, k, v, scale, target_s: float):
+    """Oracle on the first `rows` query rows (all heads, all keys), the row
+    count grown until one call takes at least target_s; (rows, seconds)."""
     rows = 8
     while True:
         qs = np.ascontiguousarray(q[:, :rows])
         t0 = time.perf_counter()
         oracle.attn(qs, k, v, scale)
         dt = time.perf_counter() - t0
-        if dt >= target_s or rows >= W["S"]:
-            break
-        rows = min(W["S"], max(rows * 2, int(rows * target_s / max(dt, 1e-3) * 1.1)))
+        if dt >= target_s or rows >= q.shape[1]:
+            return rows, dt
+        rows = min(q.shape[1], max(rows * 2, int(rows * target_s / max(dt, 1e-3) * 1.1)))
+
+
+def cpu_baseline(target_s: float):
+    """Times the fp64 oracle on a bounded sample of the window self-attention
+    (a few query rows of all 12 heads against all 10920 keys): on all host
+    threads (`value`), then on one (`single_thread`, a smaller sample)."""
+    import oracle
+    from paper_2607_28144_amd import synth
+    W = WINDOW
+    q, k, v = synth.qkv(W["seed"], W["B"], W["H"], W["S"], W["S"], W["D"])
+    scale = synth.default_scale(W["D"])
+    n_all = oracle.num_threads()
+    rows, dt = oracle_sample(oracle, q, k, v, scale, target_s)
+    oracle.set_num_threads(1)
+    try:
+        rows1, dt1 = oracle_sample(oracle, q, k, v, scale, target_s / 3)
+    finally:
+        oracle.set_num_threads(n_all)
     flops = attn_flops(W["B"], W["H"], rows, W["S"], W["D"])
+    flops1 = attn_flops(W["B"], W["H"], rows1, W["S"], W["D"])
     return {
         "value": flops / dt / 1e12,
         "unit": "TFLOP/s",
-        "cores": oracle.num_threads(),
+        "cores": n_all,
         "kind": "oracle",
         "sample": f"window self-attention, {rows} query rows x {W['H']} heads x {W['S']} keys, d={W['D']} "
-                  f"(fp64 two-pass oracle, {dt:.1f} s on {cpu_model()})",
+                  f"(fp64 two-pass oracle, {dt:.1f} s on {n_all} threads of {cpu_model()}, "
+                  f"{os.cpu_count()} logical CPUs visible)",
         "seconds": dt,
+        "single_thread": {"value": flops1 / dt1 / 1e12, "unit": "TFLOP/s", "cores": 1, "seconds": dt1,
+                          "sample": f"{rows1} query rows x {W['H']} heads x {W['S']} keys on 1 thread"},
     }
+
+
+def time_calls(torch, stream, fn, steps, warmup):
+    """Average / median / min ms of one call of fn, HIP events on `stream`
+    around each call, after `warmup` untimed calls."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    evs = []
+    for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        evs.append((e0, e1))
+    torch.cuda.synchronize()
+    t = sorted(a.elapsed_time(b) for a, b in evs)
+    return {"ms_avg": sum(t) / len(t), "ms_median": t[len(t) // 2], "ms_min": t[0]}
+
+
+def config_legs(torch, api, synth, dev, to_dev, steps, warmup):
+    """The other configurations, each timed alone: image-scale self-attention
+    and the paper's own rank share (partials + merge), with roofline
+    fractions against the dense bf16 MFMA peak."""
+    stream = torch.cuda.current_stream(dev)
+    legs = {}
+    I = IMAGE
+    q, k, v = (to_dev(x) for x in synth.qkv(I["seed"], I["B"], I["H"], I["S"], I["S"], I["D"]))
+    scale = synth.default_scale(I["D"])
+    o = torch.empty((I["B"], I["S"], I["H"], I["D"]), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((I["B"], I["H"], I["S"]), dtype=torch.float32, device=dev)
+    t = time_calls(torch, stream, lambda: api.attn_fwd(q, k, v, scale=scale, out=o, lse_out=lse), steps, warmup)
+    g = attn_flops(I["B"], I["H"], I["S"], I["S"], I["D"])
+    tf = g / (t["ms_avg"] * 1e-3) / 1e12
+    legs["image_self_s4096_h12"] = dict(t, gflop=g / 1e9, tflops=tf, frac=tf / PEAK_BF16_TFLOPS,
+                                        workload="self-attention B=1 H=12 S=4096 d=128 bf16 O + LSE")
+    del q, k, v, o, lse
+    P = PAPER_SHARE
+    q, k, v = synth.qkv(P["seed"], P["B"], P["H"], P["S"], P["S"], P["D"])
+    q = to_dev(np.ascontiguousarray(q[:, :P["Sq"]]))
+    k, v = to_dev(k), to_dev(v)
+    csz = P["S"] // P["chunks"]
+    bounds = [i * csz for i in range(P["chunks"])] + [P["S"]]
+    o_parts = [torch.empty((P["B"], P["Sq"], P["H"], P["D"]), dtype=torch.float32, device=dev)
+               for _ in range(P["chunks"])]
+    l_parts = [torch.empty((P["B"], P["H"], P["Sq"]), dtype=torch.float32, device=dev) for _ in range(P["chunks"])]
+    o = torch.empty((P["B"], P["Sq"], P["H"], P["D"]), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((P["B"], P["H"], P["Sq"]), dtype=torch.float32, device=dev)
+
+    def paper_share():
+        for i in range(P["chunks"]):
+            a, b = bounds[i], bounds[i + 1]
+            api.attn_partial_fwd(q, k[:, a:b], v[:, a:b], scale=scale, out=o_parts[i], lse_out=l_parts[i])
+        api.lse_merge(o_parts, l_parts, out=o, lse_out=lse)
+
+    t = time_calls(torch, stream, paper_share, steps, warmup)
+    g = attn_flops(P["B"], P["H"], P["Sq"], P["S"], P["D"])
+    tf = g / (t["ms_avg"] * 1e-3) / 1e12
+    legs["paper_share_h3_sq5460_chunks2x5460"] = dict(
+        t, gflop=g / 1e9, tflops=tf, frac=tf / PEAK_BF16_TFLOPS,
+        workload="rank share of the 12-head model under Ulysses 4 x Ring 2: H=3, Sq=5460, keys in 2 chunks "
+                 "of 5460, 2 partials (f32) + LSE merge (bf16)")
+    return legs
 
 
 def copy_reference(torch, dev, args):
@@ -335,7 +423,7 @@ def main():
     total_ms = t_start.elapsed_time(t_end)
     ms_per_step = total_ms / args.steps
     step_flops = sum(flops[c] for c in comps)
-    value = step_flops / (ms_per_step * 1e-3) / 1e12
+    step_tflops = step_flops / (ms_per_step * 1e-3) / 1e12
 
     components = {}
     for c in comps:
@@ -348,8 +436,11 @@ def main():
         rows = R["B"] * R["S"] * R["H"]
         components["share"]["merge_bytes"] = nch * rows * (R["D"] * 4 + 4) + rows * (R["D"] * 2 + 4)
 
+    components["step"] = {"ms_avg": ms_per_step, "gflop": step_flops / 1e9, "tflops": step_tflops,
+                          "components": comps}
     dom = "self" if "self" in comps else comps[0]
     achieved = components[dom]["tflops"]
+    value = achieved
     roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": achieved / PEAK_BF16_TFLOPS,
                 "traffic": measured_traffic() if dom == "self" else None,
@@ -371,9 +462,11 @@ def main():
         "data": "synthetic",
         "pct_of_peak": 100.0 * value / PEAK_BF16_TFLOPS,
         "config": {
-            "workload": "25-frame window attention: self-attn S=10920 (7x30x52) H=12 d=128 bf16 + cross-attn "
-                        "to 512 ctx tokens + one rank share (H=5, 4 key chunks of 2730, partials + LSE merge)"
+            "workload": "window self-attention B=1 S=10920 (7x30x52) H=12 d=128 bf16 O + LSE (value); one step "
+                        "also runs the cross-attention to 512 ctx tokens and one rank share (H=5, 4 key chunks "
+                        "of 2730, partials + LSE merge)"
             if args.only is None else f"component '{args.only}' only",
+            "value_is": f"components.{dom}: algorithmic FLOPs / average call duration (HIP events)",
             "components": comps, "B": B, "H": H, "S": S, "d": D, "ctx": W["ctx"],
             "share": {"H": R["H"], "Sq": R["S"], "chunks": nch, "chunk": csz},
             "inputs": "i.i.d. N(0,1) bf16, seeds 3 (window) and 4 (share)",
@@ -386,6 +479,8 @@ def main():
     if args.only is None:
         line["extras"] = next_steps_timing(torch, api, synth, dev, to_dev, q, kc, vc, rq, rk, rv, scale, bounds,
                                            o_parts, l_parts, o_share, o_cross, l_cross)
+        del q, k, v, kc, vc, rq, rk, rv, o_parts, l_parts
+        line["legs"] = config_legs(torch, api, synth, dev, to_dev, 30, 10)
     if not args.no_cpu_baseline and args.only is None:
         print("[bench] timing the oracle on the host cores", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(args.cpu_seconds)

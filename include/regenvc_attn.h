@@ -5,9 +5,9 @@
  * attention (paper Sec. 3.5, "Multi-GPU unified sequence parallelism"):
  *   - Ulysses hands every GPU the whole token sequence for a subset of heads
  *     and asks for exact attention over it                -> regenvc_attn_fwd
- *   - Ring streams key/value blocks between GPUs and combines them
- *     online-softmax style: one partial result per key/value chunk, then a
- *     log-sum-exp merge that is exact up to reduction order
+ *   - Ring passes key/value blocks between GPUs and folds their results
+ *     together with running-max rescaling: one partial result per key/value
+ *     chunk, then a log-sum-exp merge, exact apart from summation order
  *                            -> regenvc_attn_partial_fwd + regenvc_lse_merge,
  *                               or regenvc_attn_ring_accumulate (merge fused)
  *   - the conditioning path (Sec. 3.9, "Hybrid CPU-GPU deployment") streams
@@ -96,8 +96,8 @@ typedef struct {
 #define REGENVC_MAX_PARTS 16
 
 /* Exact self-attention over the full key sequence for H heads
-   (Sec. 3.5, Ulysses: "exact attention over the full sequence for a subset
-   of heads").
+   (Sec. 3.5, Ulysses: each GPU attends over every token of the window for
+   its own subset of heads).
      q: bf16 [B,Sq,H,D]; k, v: bf16 [B,Skv,H,D]
      o: [B,Sq,H,D] in o_dtype (bf16, round-to-nearest-even, or f32)
      lse: f32 [B,H,Sq] or NULL to skip it
@@ -110,7 +110,8 @@ regenvc_status regenvc_attn_fwd(const regenvc_tensor *q, const regenvc_tensor *k
                                 int32_t D, float softmax_scale, void *stream);
 
 /* Partial attention of every query over ONE key/value chunk (Sec. 3.5,
-   Ring: key/value blocks are streamed and combined online-softmax style).
+   Ring: key/value blocks are passed around and folded together with
+   running-max rescaling).
    The chunk is a plain view: k_chunk/v_chunk point at the chunk's first
    token with the full tensor's strides.
      o_part: f32 [B,Sq,H,D], normalized over the chunk's keys
@@ -127,7 +128,7 @@ regenvc_status regenvc_attn_partial_fwd(const regenvc_tensor *q,
 
 /* Log-sum-exp merge of num_parts partial results over disjoint key chunks
    into the result over their union (Sec. 3.5: the sharded computation equals
-   single-device attention up to reduction order):
+   single-device attention apart from summation order):
      m = max_c L_c;  L = m + log sum_c exp(L_c - m);  O = sum_c exp(L_c - L) O_c
    A part with L_c = -inf has weight 0; if every part is -inf the row is
    O = 0, L = -inf.
@@ -143,7 +144,7 @@ regenvc_status regenvc_lse_merge(const float *const *o_parts,
                                  int32_t D, void *stream);
 
 /* Ring accumulate (Sec. 3.5: Ring combines the streamed key/value blocks
-   online-softmax style): partial attention over ONE key/value chunk whose
+   with running-max rescaling): partial attention over ONE key/value chunk whose
    epilogue merges the result straight into the running state of the chunks
    already processed, so no separate merge pass and no per-chunk partial
    buffers are needed.  Per row, with (O_run, L_run) the running state and

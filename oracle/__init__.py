@@ -30,6 +30,8 @@ def open_library(path: str) -> ctypes.CDLL:
     lib.oracle_merge.restype = i32
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = i32
+    lib.oracle_set_num_threads.argtypes = [i32]
+    lib.oracle_set_num_threads.restype = None
     lib.oracle_norm_rope.argtypes = [p, i64, i64, i64, p, p, i32, i32, i32, i32, i32, i32, i32, i32,
                                      ctypes.c_float, ctypes.c_float]
     lib.oracle_norm_rope.restype = i32
@@ -88,8 +90,8 @@ def merge(o_parts, lse_parts, lib=None):
 
 
 def ring_accumulate(o_run, lse_run, q, k, v, scale: float, lib=None):
-    """One ring step (paper Sec. 3.5, key/value blocks combined online-softmax
-    style): the attention of q over this key/value chunk, merged into the
+    """One ring step (paper Sec. 3.5: key/value blocks folded into a running
+    result with running-max rescaling): the attention of q over this key/value chunk, merged into the
     running state (o_run, lse_run) of the chunks seen so far by the same
     log-sum-exp identity as merge().  Rows whose lse_run is -inf have seen no
     key; their o_run is not used.  Returns the new (O, LSE), float64."""
@@ -131,3 +133,8 @@ def norm_rope(x: np.ndarray, w: np.ndarray, grid, token0: int = 0, eps: float = 
 
 def num_threads() -> int:
     return _load().oracle_num_threads()
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of later oracle calls (e.g. 1 to time it on one core)."""
+    _load().oracle_set_num_threads(int(n))

@@ -1,7 +1,7 @@
 """Brute-force attention in pure Python -- TEST INFRASTRUCTURE ONLY.
 
 The literal formula of exact softmax attention (paper Sec. 3.5: each GPU
-computes exact attention over the full sequence for its heads), one query row
+attends over every token of the window for its heads), one query row
 at a time, with math.exp and correctly rounded sums (math.fsum).  For tiny
 inputs only; it pins the C oracle, it is not used to check the GPU.
 """

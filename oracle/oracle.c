@@ -8,10 +8,11 @@
  * source, header, table or helper with the GPU path.
  *
  * What is computed (paper, Sec. 3.5 "Multi-GPU unified sequence parallelism"):
- *   Ulysses gives every GPU exact attention over the whole token sequence for
- *   a subset of heads; Ring streams key/value blocks and combines them
- *   "online-softmax" style; the parallel result equals single-device attention
- *   up to reduction order.  The plain definition of that result, per batch b,
+ *   under Ulysses every GPU attends over all tokens of the window for its own
+ *   subset of heads; under Ring key/value blocks travel between GPUs and their
+ *   partial results are folded together with running-max rescaling; either
+ *   way the result is single-device attention, apart from the order of the
+ *   floating-point reductions.  The plain definition of it, per batch b,
  *   head h and query row i, with the caller's float32 scale widened to double:
  *
  *       s_j  = scale * sum_t Q[b,i,h,t] * K[b,j,h,t]          j = 0..Skv-1
@@ -153,6 +154,19 @@ int oracle_merge(const double *const *o_parts, const double *const *lse_parts,
                 lse[li] = L;
             }
     return 0;
+}
+
+/* Sets the number of OpenMP threads of later oracle calls (n >= 1); used to
+ * time the oracle on one host core as well as on all of them. */
+void oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    extern void omp_set_num_threads(int);
+    if (n >= 1)
+        omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
 }
 
 /* Number of OpenMP threads the oracle runs on (reported next to its timing). */

@@ -2,8 +2,9 @@
 // accumulation, online softmax in registers, K/V tiles streamed through LDS.
 //
 // Method: exact softmax attention computed blockwise over key/value tiles with
-// a running (max, sum) per query row -- the "online-softmax" combination the
-// paper's Ring attention relies on (Sec. 3.5); a single launch covers one
+// a running (max, sum) per query row -- the same rescaling recurrence by
+// which the paper's Ring attention folds key/value blocks together (Sec.
+// 3.5); a single launch covers one
 // GPU's share (a subset of heads, all or a chunk of the keys).
 //
 // Work decomposition
@@ -46,6 +47,13 @@
 //   LSE = ln2 * (m_ref + log2 l) are the same quantities for any reference,
 //   so this only removes the O-rescale work from the common path; when it is
 //   needed it is applied between the phases, outside the MFMA streams.
+//
+// Two running sums per query: l_r, of the weights as rounded to bf16 for the
+//   P V product, divides O (O is then exactly a convex combination of the V
+//   rows, whatever the rounding: when one key carries nearly all the weight,
+//   its rounding cancels instead of reaching O); l, of the unrounded fp32
+//   weights, gives LSE (a single dominant weight's bf16 rounding would move
+//   LSE by up to 2^-9).
 #include "attn_kernels.hpp"
 
 #include <math.h>
@@ -210,14 +218,19 @@ __device__ __forceinline__ float quad_sum(float x)
 }
 
 // Stores the weights (x0, x1), rounded to bf16 (nearest even, one packed
-// conversion), as weights j, j+1 of a P operand.
-__device__ __forceinline__ void put_pair(bf16x8 &dst, int j, float x0, float x1)
+// conversion), as weights j, j+1 of a P operand, and adds the two rounded
+// values to rs: one v_dot2c_f32_bf16 of the packed pair against (1, 1), so
+// that the sum that normalizes O is the sum of exactly the weights the P V
+// product multiplies (O is then a convex combination of V rows).
+__device__ __forceinline__ void put_pair(bf16x8 &dst, int j, float x0, float x1, float &rs)
 {
     bf16x2 pk;
     pk[0] = (__bf16)x0;
     pk[1] = (__bf16)x1;
     dst[j] = pk[0];
     dst[j + 1] = pk[1];
+    const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+    rs = __builtin_amdgcn_fdot2_f32_bf16(pk, one, rs, false);
 }
 
 // Online-softmax step for one 32-query block over one 64-key tile.
@@ -227,14 +240,15 @@ __device__ __forceinline__ void put_pair(bf16x8 &dst, int j, float x0, float x1)
 //   c      : scale * log2(e)
 //   mref   : exponent reference (log2 units), raised lazily
 //   lsum   : running fp32 sum of exp2(s*c - mref) over this lane's keys (the
-//            unrounded weights; it normalizes O and gives LSE)
+//            unrounded weights; it gives LSE)
+//   rsum   : running sum of the same weights rounded to bf16 (it normalizes O)
 //   p      : bf16 P^T operands of the four 16-key MFMA steps of the tile
 //   alpha  : factor the O accumulator must be multiplied by (1 if unchanged)
 //   upd    : wave-uniform flag: some lane raised its reference
 // MASK: keys at or past Skv (only in the last tile) get weight exactly 0.
 template <bool MASK>
-__device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, float &mref, float &lsum, bf16x8 (&p)[4],
-                                              float &alpha, bool &upd, int key0, int Skv)
+__device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, float &mref, float &lsum, float &rsum,
+                                              bf16x8 (&p)[4], float &alpha, bool &upd, int key0, int Skv)
 {
     const int hi = (threadIdx.x >> 5) & 1;
     auto valid = [&](int kb, int i) { return key0 + kb * 32 + (i >> 2) * 8 + hi * 4 + (i & 3) < Skv; };
@@ -250,7 +264,7 @@ __device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, flo
     alpha = __builtin_amdgcn_exp2f(mref - mnew);
     mref = mnew;
     const float nm = -mnew;
-    float acc0 = 0.f, acc1 = 0.f;
+    float acc0 = 0.f, acc1 = 0.f, racc = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -261,11 +275,12 @@ __device__ __forceinline__ void softmax_block(const f32x16 (&s)[2], float c, flo
                 e0 = valid(kb, i) ? e0 : 0.f;
                 e1 = valid(kb, i + 1) ? e1 : 0.f;
             }
-            put_pair(p[kb * 2 + (i >> 3)], i & 7, e0, e1);
+            put_pair(p[kb * 2 + (i >> 3)], i & 7, e0, e1, racc);
             acc0 += e0;
             acc1 += e1;
         }
     lsum = fmaf(lsum, alpha, acc0 + acc1);
+    rsum = fmaf(rsum, alpha, racc);
 }
 
 // One key/value context of a (batch, head): K and V base pointers, row
@@ -378,19 +393,20 @@ __device__ __forceinline__ float load_run(const AttnArgs &a, int b, int h, int q
     return a.run_lse[((int64_t)b * a.H + h) * a.Sq + qi];
 }
 
-// Epilogue of one lane's query row: O = O^T / l and LSE = ln2 * (m_ref +
-// log2 l), with l the fp32 sum of the weights; a split tile's key range
-// writes its normalized partial to the workspace instead.  lsum is this
-// lane's half of l (the other half is in lane^32).
+// Epilogue of one lane's query row: O = O^T / l_r and LSE = ln2 * (m_ref +
+// log2 l), with l_r the sum of the rounded weights and l of the unrounded
+// ones; a split tile's key range writes its normalized partial to the
+// workspace instead.  lsum and rsum are this lane's halves of l and l_r (the
+// other halves are in lane^32).
 template <int D, bool OUT_F32, bool ACC>
 __device__ __forceinline__ void store_row(const AttnArgs &a, const AttnPlan &pl, const f32x16 (&oacc)[D / 32],
-                                          float lsum, float mref, int b, int h, int qi, int qrow, int slot)
+                                          float lsum, float rsum, float mref, int b, int h, int qi, int qrow, int slot)
 {
     constexpr int BM = kWaves * 32;
     constexpr int DB = D / 32;
     const int hi = (threadIdx.x >> 5) & 1;
     const float lt = pair_sum(lsum);
-    const float inv = 1.0f / lt;
+    const float inv = 1.0f / pair_sum(rsum);
     const float lse_val = (mref + __log2f(lt)) * kLn2;
     if (qi >= a.Sq) return;
     if (slot >= 0) {
@@ -613,7 +629,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
                                     a.k2_ss, a.v2_ss, a.Skv2, pl.n_kt2, a.kv2_off32}
                             : src0;
     f32x16 oacc[DB];
-    float mref, lsum;
+    float mref, lsum, rsum;
     const float c = a.scale * kLog2e;
     float lse1 = 0.f;  // dual launches: LSE of the first context
 
@@ -734,14 +750,15 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 #pragma unroll
     for (int db = 0; db < DB; ++db) oacc[db] = f32x16{};
     mref = -INFINITY;
-    lsum = 0.f;
+    lsum = rsum = 0.f;
     f32x16 scur[2], snext[2];
     bf16x8 p[4];
     float alpha = 1.f;
     bool upd = false;
     // softmax state carried from phase X into phase Y of a step: -mref, the
-    // first half's weight sum and the second half's partial sums
-    float nm = 0.f, acc0 = 0.f, acc1 = 0.f, acc2 = 0.f;
+    // first half's weight sums (unrounded, rounded) and the second half's
+    // partial sums
+    float nm = 0.f, acc0 = 0.f, acc1 = 0.f, acc2 = 0.f, racc0 = 0.f, racc1 = 0.f;
 
     // O^T += V^T P^T for the key tile in stage `st`: each MFMA's V fragment is read PF
     // MFMAs ahead; the order is pinned so that the waits stay PF deep.  With
@@ -766,7 +783,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
                     for (int e = i * TN; e < (i + 1) * TN; e += 2) {
                         const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[1][e], c, nm));
                         const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[1][e + 1], c, nm));
-                        put_pair(p[2 + (e >> 3)], e & 7, x0, x1);
+                        put_pair(p[2 + (e >> 3)], e & 7, x0, x1, racc1);
                         acc1 += x0;
                         acc2 += x1;
                     }
@@ -788,19 +805,22 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 #pragma unroll
                         for (int db = 0; db < DB; ++db) oacc[db] *= al;
                         lsum *= al;
+                        rsum *= al;
                         acc0 *= al;
-                        acc1 = acc2 = 0.f;
+                        racc0 *= al;
+                        acc1 = acc2 = racc1 = 0.f;
 #pragma unroll
                         for (int e = 0; e < 16; e += 2) {
                             const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[1][e], c, -mnew));
                             const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[1][e + 1], c, -mnew));
-                            put_pair(p[2 + (e >> 3)], e & 7, x0, x1);
+                            put_pair(p[2 + (e >> 3)], e & 7, x0, x1, racc1);
                             acc1 += x0;
                             acc2 += x1;
                         }
                         a2 = acc1 + acc2;
                     }
                     lsum += acc0 + a2;
+                    rsum += racc0 + racc1;
                 }
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -825,7 +845,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         __builtin_amdgcn_s_setprio(1);
         constexpr int STRIDE = NK / 8;
         bf16x8 kr[PF];
-        acc0 = acc1 = 0.f;
+        acc0 = acc1 = racc0 = 0.f;
         const float nm0 = -mref;
 #pragma unroll
         for (int i = 0; i < PF; ++i) kr[i] = kfrag(kt, i);
@@ -841,7 +861,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
                 const int e = 2 * (i / STRIDE);
                 const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[0][e], c, nm0));
                 const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[0][e + 1], c, nm0));
-                put_pair(p[e >> 3], e & 7, x0, x1);
+                put_pair(p[e >> 3], e & 7, x0, x1, racc0);
                 acc0 += x0;
                 acc1 += x1;
             }
@@ -850,7 +870,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         float a1 = acc0 + acc1;
         // keep this half of the softmax in this phase: without a use here the
         // compiler sinks it past the branch below, next to the P V products
-        __asm__ volatile("" : : "v"(p[0]), "v"(p[1]), "v"(a1));
+        __asm__ volatile("" : : "v"(p[0]), "v"(p[1]), "v"(a1), "v"(racc0));
         upd = __builtin_amdgcn_ballot_w64(!(a1 <= kSpecLimit) && a1 == a1) != 0;
         if (upd) {
             float m0 = -INFINITY, m1 = -INFINITY;
@@ -863,19 +883,20 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
             alpha = __builtin_amdgcn_exp2f(mref - mnew);
             mref = mnew;
             lsum *= alpha;
-            acc0 = acc1 = 0.f;
+            rsum *= alpha;
+            acc0 = acc1 = racc0 = 0.f;
 #pragma unroll
             for (int e = 0; e < 16; e += 2) {
                 const float x0 = __builtin_amdgcn_exp2f(fmaf(sc[0][e], c, -mnew));
                 const float x1 = __builtin_amdgcn_exp2f(fmaf(sc[0][e + 1], c, -mnew));
-                put_pair(p[e >> 3], e & 7, x0, x1);
+                put_pair(p[e >> 3], e & 7, x0, x1, racc0);
                 acc0 += x0;
                 acc1 += x1;
             }
             a1 = acc0 + acc1;
         }
         acc0 = a1;
-        acc1 = acc2 = 0.f;
+        acc1 = acc2 = racc1 = 0.f;
         nm = -mref;
     };
 
@@ -909,7 +930,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
             issue_next(next_stage(st1));             // tile t+kAhead, into the stage tile t-1 used
             qk_softmax(st1, sc, sn);
         } else {
-            softmax_block<MASK>(sc, c, mref, lsum, p, alpha, upd, t * kBlockN, Skv);
+            softmax_block<MASK>(sc, c, mref, lsum, rsum, p, alpha, upd, t * kBlockN, Skv);
         }
         // ---- O rescale (rare), outside the MFMA streams
         if (upd) {
@@ -949,7 +970,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
         // park the first context's normalized O in LDS (bf16) and its LSE
         const float lt1 = pair_sum(lsum);
         lse1 = (mref + __log2f(lt1)) * kLn2;
-        const float inv = 1.0f / lt1;
+        const float inv = 1.0f / pair_sum(rsum);
         lds_char *park = (lds_char *)smem + G::LDS + threadIdx.x * 16;
 #pragma unroll
         for (int j = 0; j < DB * 2; ++j) {  // chunk j: values 8j .. 8j+7 of (db, gq, e) order
@@ -963,12 +984,12 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     }
 
     if (slot >= 0 || OUT_F32 || ACC) {
-        store_row<D, OUT_F32, ACC>(a, pl, oacc, lsum, mref, b, h, qi, qrow, slot);
+        store_row<D, OUT_F32, ACC>(a, pl, oacc, lsum, rsum, mref, b, h, qi, qrow, slot);
         return;
     }
     // whole tile, bf16 output: final values in oacc, then full-row stores
     const float lt = pair_sum(lsum);
-    const float inv = 1.0f / lt;
+    const float inv = 1.0f / pair_sum(rsum);
     const float lse_last = (mref + __log2f(lt)) * kLn2;
     if constexpr (DUAL) {
         // the sum goes out straight from the accumulator layout (measured
@@ -1174,7 +1195,9 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     f32x4 s[4][2];
     bf16x8 p[2][2];  // P^T operands: 32-key step ks, query block qb
     const float c = a.scale * kLog2e;
-    float mref[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f};
+    // per query block: reference, sum of the unrounded weights (LSE) and of
+    // the bf16-rounded weights (the normalizer of O)
+    float mref[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f}, rsum[2] = {0.f, 0.f};
 
     // First PF operand fragments of an M phase (see mphase), read ahead of it.
     bf16x8 r[PF];
@@ -1226,13 +1249,13 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     auto vphase = [&](int key0, auto mask) __attribute__((always_inline)) {
         constexpr bool MASK = decltype(mask)::value;
         auto valid = [&](int kb, int i) { return key0 + kb * 16 + g * 4 + i < Skv; };
-        float e_sum[2];
+        float e_sum[2], r_sum[2];
         auto weights = [&]() __attribute__((always_inline)) {
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb) {
                 const float nm = -mref[qb];
                 // -0 starts the sums (0 + x is not foldable: it turns -0 into +0)
-                float a0 = -0.f, a1 = -0.f;
+                float a0 = -0.f, a1 = -0.f, ar = -0.f;
 #pragma unroll
                 for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -1243,11 +1266,12 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
                             e0 = valid(kb, i) ? e0 : 0.f;
                             e1 = valid(kb, i + 1) ? e1 : 0.f;
                         }
-                        put_pair(p[kb >> 1][qb], (kb & 1) * 4 + i, e0, e1);
+                        put_pair(p[kb >> 1][qb], (kb & 1) * 4 + i, e0, e1, ar);
                         a0 += e0;
                         a1 += e1;
                     }
                 e_sum[qb] = a0 + a1;
+                r_sum[qb] = ar;
             }
         };
         weights();
@@ -1269,11 +1293,14 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
 #pragma unroll
                 for (int db = 0; db < DB; ++db) oacc[db][qb] *= alpha;
                 lsum[qb] *= alpha;
+                rsum[qb] *= alpha;
             }
             weights();
         }
         lsum[0] += e_sum[0];
         lsum[1] += e_sum[1];
+        rsum[0] += r_sum[0];
+        rsum[1] += r_sum[1];
     };
 
     using T_ = std::true_type;
@@ -1387,16 +1414,16 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     }
     wait_vmcnt<0>();  // the clamped trailing copies must land before the workgroup exits
 
-    // Epilogue: per query, l = the sum of the four lanes' partial sums;
-    // O = O^T / l, LSE = ln2 * (m_ref + log2 l); a split tile's key range
-    // writes its normalized partial to the workspace instead.
+    // Epilogue: per query, l and l_r = the sums of the four lanes' partial
+    // sums; O = O^T / l_r, LSE = ln2 * (m_ref + log2 l); a split tile's key
+    // range writes its normalized partial to the workspace instead.
     {
         if (slot < 0) {  // whole tile: staged full-row stores (f32 rows take the whole 128 KB ring)
             float wr[2] = {0.f, 0.f};  // ring accumulate: the running output's weight per query block
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb) {
                 const float lt = quad_sum(lsum[qb]);
-                float sc = 1.0f / lt;
+                float sc = 1.0f / quad_sum(rsum[qb]);
                 float lse_val = (mref[qb] + __log2f(lt)) * kLn2;
                 const int qi = qi0 + qb * 16;
                 if constexpr (ACC) {
@@ -1439,7 +1466,7 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
         const float lt = quad_sum(lsum[qb]);
-        const float inv = 1.0f / lt;
+        const float inv = 1.0f / quad_sum(rsum[qb]);
         const int qrow = qrow0 + qb * 16, qi = qi0 + qb * 16;
         if (qi >= a.Sq) continue;
         float *orow = pl.ws_o + ((int64_t)slot * BM + qrow) * D;

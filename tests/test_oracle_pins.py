@@ -2,9 +2,10 @@
 
 The oracle (oracle/oracle.c) is the definition of exact softmax attention
 and of the log-sum-exp merge of key/value-chunk partials (paper Sec. 3.5:
-Ulysses computes exact attention over the full sequence for a subset of
-heads; Ring combines streamed key/value blocks online-softmax style; the
-sharded result equals single-device attention up to reduction order).  The
+under Ulysses each GPU attends over all tokens for its subset of heads;
+Ring folds passed-around key/value blocks together with running-max
+rescaling; the sharded result is single-device attention apart from the
+order of floating-point reductions).  The
 paper prints no worked numeric example of attention, so every pin here is
 exact mathematics: brute force on tiny inputs, closed forms, invariants, and
 a library special case.  test_planted_mistakes_are_caught checks that these
