@@ -29,12 +29,16 @@
  *     whole rounds of the GPU's compute units, the leftover tiles are split
  *     along the keys and their partial results combined by a second kernel.
  *     Those partials live in a workspace of (split units) x 256 x (D + 1)
- *     floats (15.3 MB for 12 heads x 10920 tokens at D = 128) that the call
- *     takes, stream-ordered, from a per-device memory pool and returns to it,
- *     stream-ordered, before it returns; the pool keeps that memory for
- *     later calls until the process ends.  A failed pool allocation returns
- *     REGENVC_ERR_HIP with nothing enqueued.  regenvc_lse_merge allocates
- *     nothing.
+ *     floats (15.3 MB for 12 heads x 10920 tokens at D = 128; the exact size
+ *     of a call is workspace_bytes of regenvc_attn_plan_query or
+ *     regenvc_cross_attn_dual_plan_query).  A caller that binds a workspace
+ *     with regenvc_attn_set_workspace supplies it and the library allocates
+ *     nothing.  Otherwise the call takes it, stream-ordered, from a
+ *     per-device memory pool and returns it, stream-ordered, before it
+ *     returns; the pool keeps that memory for later calls until the process
+ *     ends, and a failed pool allocation returns REGENVC_ERR_HIP with
+ *     nothing enqueued.  regenvc_lse_merge and regenvc_qk_norm_rope use no
+ *     scratch.
  *   - Q/K/V/O are logical [B, S, H, D] with element strides for b, s and h
  *     (regenvc_tensor); the D axis is contiguous.  Token-major [B,S,H,D]
  *     and head-major [B,H,S,D] are both expressible.  Inputs are bf16.
@@ -268,6 +272,36 @@ typedef struct {
 
 regenvc_status regenvc_attn_plan_query(int32_t B, int32_t H, int32_t Sq, int32_t Skv, int32_t D,
                                        int32_t n_cu, regenvc_attn_plan *plan);
+
+/* Work plan of one regenvc_cross_attn_dual_fwd call: as
+   regenvc_attn_plan_query, with key_tiles the tiles of both contexts and
+   key_ranges the ranges of a split tile over both (S_txt, S_img >= 1). */
+regenvc_status regenvc_cross_attn_dual_plan_query(int32_t B, int32_t H, int32_t Sq, int32_t S_txt,
+                                                  int32_t S_img, int32_t D, int32_t n_cu,
+                                                  regenvc_attn_plan *plan);
+
+/* Binds a caller-owned DEVICE buffer of `bytes` bytes as the scratch memory
+   of the attention calls (regenvc_attn_fwd, regenvc_attn_partial_fwd,
+   regenvc_attn_ring_accumulate, regenvc_cross_attn_fwd,
+   regenvc_cross_attn_dual_fwd) made later on the calling thread, until
+   another binding replaces it; workspace == NULL unbinds (back to the pool).
+   While a buffer is bound those calls allocate nothing.  A call that needs
+   more than `bytes` (its plan's workspace_bytes on the current device)
+   returns REGENVC_ERR_INVALID_ARG and enqueues nothing, as does one whose
+   tensors overlap the part of the buffer it would use.  Each call uses the
+   buffer stream-ordered on its own stream: calls that share it must be
+   ordered (one stream, or synchronized), since concurrent calls on
+   different streams would overwrite each other's partials.  The library
+   never frees or keeps the buffer beyond the binding.
+     workspace: 256-byte aligned (else REGENVC_ERR_UNSUPPORTED), or NULL
+     bytes >= 0 (else REGENVC_ERR_INVALID_ARG; ignored when unbinding)
+   Host-only: makes no HIP call. */
+regenvc_status regenvc_attn_set_workspace(void *workspace, int64_t bytes);
+
+/* Number of attention calls in this process (all threads and devices) that
+   took their scratch from the library's pool; a diagnostic for callers and
+   tests that must not allocate.  Host-only. */
+int64_t regenvc_attn_pool_draws(void);
 
 /* Static text for a status code. */
 const char *regenvc_status_str(regenvc_status status);

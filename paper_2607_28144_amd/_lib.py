@@ -47,6 +47,8 @@ _SIGNATURES = {
     "regenvc_cross_attn_fwd": [_PT, _PT, _PT, _PT, ctypes.c_int, ctypes.c_void_p,
                                _i32, _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_void_p],
     "regenvc_attn_plan_query": [_i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(AttnPlan)],
+    "regenvc_cross_attn_dual_plan_query": [_i32, _i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(AttnPlan)],
+    "regenvc_attn_set_workspace": [ctypes.c_void_p, ctypes.c_int64],
     "regenvc_qk_norm_rope": [_PT, _PT, ctypes.c_void_p, ctypes.c_void_p, _PT, _PT, _i32, _i32, _i32, _i32,
                              _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_float, ctypes.c_void_p],
 }
@@ -72,6 +74,8 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.regenvc_status_str.restype = ctypes.c_char_p
     lib.regenvc_last_error.argtypes = []
     lib.regenvc_last_error.restype = ctypes.c_char_p
+    lib.regenvc_attn_pool_draws.argtypes = []
+    lib.regenvc_attn_pool_draws.restype = ctypes.c_int64
     if path is None:
         _lib = lib
     return lib

@@ -3,7 +3,10 @@
 Every step of the computation runs in the HIP kernels of libregenvc_attn.so;
 torch supplies device memory and the current stream.  Tensors are logical
 [B, S, H, D] views (any b/s/h strides that are multiples of 8 elements, d
-contiguous); LSE tensors are float32 [B, H, Sq].
+contiguous); LSE tensors are float32 [B, H, Sq].  The scratch memory of the
+attention calls (split-tile partials, sized by the call's work plan) is
+allocated by torch on the current stream and bound for the call, so the
+library itself never allocates on this path.
 """
 from __future__ import annotations
 
@@ -49,6 +52,60 @@ def _scale(scale: Optional[float], D: int) -> float:
     return float(torch.tensor(1.0 / math.sqrt(D), dtype=torch.float32)) if scale is None else float(scale)
 
 
+_NEED = {}    # (device index, shape) -> workspace bytes of the call's plan
+_N_CU = {}    # device index -> compute units
+_TOKEN = {}   # device index -> a 256-byte buffer bound when a call needs no scratch
+
+
+def _workspace_need(device: torch.device, B, H, Sq, Skv, D, Skv2: int = 0) -> int:
+    """Scratch bytes of one attention call (the library's host-only plan query
+    with this device's compute-unit count)."""
+    idx = device.index if device.index is not None else torch.cuda.current_device()
+    key = (idx, B, H, Sq, Skv, Skv2, D)
+    need = _NEED.get(key)
+    if need is None:
+        if idx not in _N_CU:
+            _N_CU[idx] = torch.cuda.get_device_properties(idx).multi_processor_count
+        if Skv < 1 or B * H * Sq == 0:
+            need = 0
+        else:
+            plan = _lib.AttnPlan()
+            lib = _lib.load()
+            if Skv2 > 0:
+                st = lib.regenvc_cross_attn_dual_plan_query(B, H, Sq, Skv, Skv2, D, _N_CU[idx], ctypes.byref(plan))
+            else:
+                st = lib.regenvc_attn_plan_query(B, H, Sq, Skv, D, _N_CU[idx], ctypes.byref(plan))
+            need = plan.workspace_bytes if st == _lib.OK else 0
+        _NEED[key] = need
+    return need
+
+
+def _with_workspace(device: torch.device, need: int, call):
+    """Runs call() (one attention entry point) with a torch-allocated scratch
+    buffer of `need` bytes bound: the library then allocates nothing.  When
+    the call needs none, a small token buffer is bound instead, so that a
+    plan mismatch fails loudly rather than falling back to the pool."""
+    lib = _lib.load()
+    if need > 0:
+        buf = torch.empty(need, dtype=torch.uint8, device=device)
+    else:
+        idx = device.index if device.index is not None else torch.cuda.current_device()
+        buf = _TOKEN.get(idx)
+        if buf is None:
+            buf = _TOKEN[idx] = torch.empty(256, dtype=torch.uint8, device=device)
+    _lib.check(lib.regenvc_attn_set_workspace(buf.data_ptr(), need), "regenvc_attn_set_workspace")
+    try:
+        return call()
+    finally:
+        lib.regenvc_attn_set_workspace(None, 0)
+
+
+def pool_draws() -> int:
+    """Attention calls in this process that took scratch from the library's
+    own pool (regenvc_attn_pool_draws); the calls of this binding never do."""
+    return int(_lib.load().regenvc_attn_pool_draws())
+
+
 def _attn(fn_name: str, q, k, v, scale, out_dtype, out, want_lse, lse_out):
     B, Sq, H, D = q.shape
     Skv = k.shape[1]
@@ -62,13 +119,16 @@ def _attn(fn_name: str, q, k, v, scale, out_dtype, out, want_lse, lse_out):
     od = _desc(out, "out", out_dtype)
     lp = _fptr(lse_out, "lse", (B, H, Sq))
     lib = _lib.load()
+    need = _workspace_need(q.device, B, H, Sq, Skv, D)
     with torch.cuda.device(q.device):
         if fn_name == "regenvc_attn_partial_fwd":
-            st = lib.regenvc_attn_partial_fwd(ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), ctypes.byref(od),
-                                              lp, B, H, Sq, Skv, D, _scale(scale, D), _stream(q.device))
+            st = _with_workspace(q.device, need, lambda: lib.regenvc_attn_partial_fwd(
+                ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), ctypes.byref(od), lp, B, H, Sq, Skv, D,
+                _scale(scale, D), _stream(q.device)))
         else:
-            st = getattr(lib, fn_name)(ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), ctypes.byref(od),
-                                       _DT[out_dtype], lp, B, H, Sq, Skv, D, _scale(scale, D), _stream(q.device))
+            st = _with_workspace(q.device, need, lambda: getattr(lib, fn_name)(
+                ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), ctypes.byref(od), _DT[out_dtype], lp, B, H,
+                Sq, Skv, D, _scale(scale, D), _stream(q.device)))
     _lib.check(st, fn_name)
     return out, lse_out
 
@@ -116,10 +176,12 @@ def attn_ring_accumulate(q: torch.Tensor, k_chunk: torch.Tensor, v_chunk: torch.
             raise ValueError(f"out shape {tuple(out.shape)} does not match q {tuple(q.shape)}")
         od, dt, res = _desc(out, "out", out_dtype), _DT[out_dtype], out
     lib = _lib.load()
+    need = _workspace_need(q.device, B, H, Sq, Skv, D)
     with torch.cuda.device(q.device):
-        st = lib.regenvc_attn_ring_accumulate(ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), ctypes.byref(rd),
-                                              lp, ctypes.byref(od) if od is not None else None, dt, B, H, Sq, Skv, D,
-                                              _scale(scale, D), _stream(q.device))
+        st = _with_workspace(q.device, need, lambda: lib.regenvc_attn_ring_accumulate(
+            ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), ctypes.byref(rd), lp,
+            ctypes.byref(od) if od is not None else None, dt, B, H, Sq, Skv, D, _scale(scale, D),
+            _stream(q.device)))
     _lib.check(st, "regenvc_attn_ring_accumulate")
     return res
 
@@ -153,11 +215,12 @@ def cross_attn_dual_fwd(q: torch.Tensor, k_txt: torch.Tensor, v_txt: torch.Tenso
              [(q, "q"), (k_txt, "k_txt"), (v_txt, "v_txt"), (k_img, "k_img"), (v_img, "v_img"), (out, "out")]]
     lt, li = _fptr(lse_txt, "lse_txt", (B, H, Sq)), _fptr(lse_img, "lse_img", (B, H, Sq))
     lib = _lib.load()
+    need = _workspace_need(q.device, B, H, Sq, St, D, Skv2=Si)
     with torch.cuda.device(q.device):
-        st = lib.regenvc_cross_attn_dual_fwd(ctypes.byref(descs[0]), ctypes.byref(descs[1]), ctypes.byref(descs[2]),
-                                             St, ctypes.byref(descs[3]), ctypes.byref(descs[4]), Si,
-                                             ctypes.byref(descs[5]), lt, li, B, H, Sq, D, _scale(scale, D),
-                                             _stream(q.device))
+        st = _with_workspace(q.device, need, lambda: lib.regenvc_cross_attn_dual_fwd(
+            ctypes.byref(descs[0]), ctypes.byref(descs[1]), ctypes.byref(descs[2]), St, ctypes.byref(descs[3]),
+            ctypes.byref(descs[4]), Si, ctypes.byref(descs[5]), lt, li, B, H, Sq, D, _scale(scale, D),
+            _stream(q.device)))
     _lib.check(st, "regenvc_cross_attn_dual_fwd")
     return out, lse_txt, lse_img
 
@@ -195,13 +258,19 @@ def lse_merge(o_parts: Sequence[torch.Tensor], lse_parts: Sequence[torch.Tensor]
     return out, lse_out
 
 
-def attn_plan(B: int, H: int, Sq: int, Skv: int, D: int, n_cu: int = 256) -> dict:
+def attn_plan(B: int, H: int, Sq: int, Skv: int, D: int, n_cu: int = 256, Skv2: int = 0) -> dict:
     """Work plan of one attention call of this shape on n_cu compute units
-    (regenvc_attn_plan_query; host-only): query/key tile counts, whole and
+    (regenvc_attn_plan_query, or regenvc_cross_attn_dual_plan_query with a
+    second context of Skv2 keys; host-only): query/key tile counts, whole and
     split query tiles, key ranges per split tile, workspace bytes."""
     plan = _lib.AttnPlan()
-    st = _lib.load().regenvc_attn_plan_query(B, H, Sq, Skv, D, n_cu, ctypes.byref(plan))
-    _lib.check(st, "regenvc_attn_plan_query")
+    lib = _lib.load()
+    if Skv2:
+        st = lib.regenvc_cross_attn_dual_plan_query(B, H, Sq, Skv, Skv2, D, n_cu, ctypes.byref(plan))
+        _lib.check(st, "regenvc_cross_attn_dual_plan_query")
+    else:
+        st = lib.regenvc_attn_plan_query(B, H, Sq, Skv, D, n_cu, ctypes.byref(plan))
+        _lib.check(st, "regenvc_attn_plan_query")
     return {f: getattr(plan, f) for f, _ in _lib.AttnPlan._fields_}
 
 

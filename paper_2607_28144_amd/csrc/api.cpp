@@ -16,6 +16,9 @@
 namespace {
 
 thread_local char g_last_error[512] = "";
+// Caller workspace bound on this thread (regenvc_attn_set_workspace).
+thread_local void *g_ws_ptr = nullptr;
+thread_local int64_t g_ws_bytes = 0;
 
 regenvc_status fail(regenvc_status st, const char *fmt, ...)
 {
@@ -216,8 +219,8 @@ regenvc_status attn_common(const char *fn, const regenvc_tensor *q, const regenv
         if (overlap(el, eq) || overlap(el, eo) || (Skv > 0 && (overlap(el, ek) || overlap(el, ev))))
             return fail(REGENVC_ERR_INVALID_ARG, "%s: lse overlaps another tensor", fn);
     }
+    Extent ek2{0, 0}, ev2{0, 0}, er{0, 0};
     if (ctx2 != nullptr) {
-        Extent ek2, ev2;
         if ((st = check_view("k_img", ctx2->k, B, ctx2->S, H, D, 2, &ek2)) != REGENVC_OK) return st;
         if ((st = check_view("v_img", ctx2->v, B, ctx2->S, H, D, 2, &ev2)) != REGENVC_OK) return st;
         if (overlap(eo, ek2) || overlap(eo, ev2))
@@ -235,7 +238,6 @@ regenvc_status attn_common(const char *fn, const regenvc_tensor *q, const regenv
         }
     }
     if (run_o != nullptr) {
-        Extent er;
         if ((st = check_view("o_run", run_o, B, Sq, H, D, 4, &er)) != REGENVC_OK) return st;
         if (!view_is_injective(run_o, B, Sq, H, D))
             return fail(REGENVC_ERR_INVALID_ARG, "%s: o_run has overlapping rows (strides)", fn);
@@ -293,7 +295,26 @@ regenvc_status attn_common(const char *fn, const regenvc_tensor *q, const regenv
         a.run_lse = lse;
         a.r_sb = run_o->stride_b, a.r_ss = run_o->stride_s, a.r_sh = run_o->stride_h;
     }
-    return launched(regenvc::launch_attn(a, static_cast<hipStream_t>(stream)), fn);
+    // split-tile partials: the workspace bound on this thread, else the pool
+    regenvc::Workspace ws{};
+    if (g_ws_ptr != nullptr) {
+        const size_t need = regenvc::attn_workspace_need(a);
+        if ((size_t)g_ws_bytes < need)
+            return fail(REGENVC_ERR_INVALID_ARG, "%s: the bound workspace holds %lld bytes, this call needs %zu", fn,
+                        (long long)g_ws_bytes, need);
+        if (need > 0) {
+            const Extent ew = flat_extent(g_ws_ptr, (int64_t)need, 1);
+            const bool hit = overlap(ew, eq) || overlap(ew, ek) || overlap(ew, ev) || overlap(ew, eo) ||
+                             overlap(ew, ek2) || overlap(ew, ev2) || overlap(ew, er) ||
+                             (lse != nullptr && overlap(ew, flat_extent(lse, (int64_t)B * H * Sq, 4))) ||
+                             (ctx2 != nullptr && ctx2->lse != nullptr &&
+                              overlap(ew, flat_extent(ctx2->lse, (int64_t)B * H * Sq, 4)));
+            if (hit) return fail(REGENVC_ERR_INVALID_ARG, "%s: the bound workspace overlaps a tensor of the call", fn);
+        }
+        ws.ptr = g_ws_ptr;
+        ws.bytes = (size_t)g_ws_bytes;
+    }
+    return launched(regenvc::launch_attn(a, static_cast<hipStream_t>(stream), ws), fn);
 }
 
 }  // namespace
@@ -482,25 +503,67 @@ regenvc_status regenvc_qk_norm_rope(const regenvc_tensor *q_in, const regenvc_te
     return launched(regenvc::launch_norm_rope(a, static_cast<hipStream_t>(stream)), fn);
 }
 
+namespace {
+
+regenvc_status plan_query(const char *fn, int32_t B, int32_t H, int32_t Sq, int32_t Skv, int32_t Skv2, int32_t D,
+                          int32_t n_cu, regenvc_attn_plan *plan)
+{
+    if (plan == nullptr) return fail(REGENVC_ERR_INVALID_ARG, "%s: plan is NULL", fn);
+    if (B < 0 || H < 0 || Sq < 0)
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: negative size (B=%d H=%d Sq=%d)", fn, B, H, Sq);
+    if (Skv < 1) return fail(REGENVC_ERR_INVALID_ARG, "%s: key count %d < 1", fn, Skv);
+    if (Skv2 < 0) return fail(REGENVC_ERR_INVALID_ARG, "%s: second key count %d < 1", fn, Skv2);
+    if (n_cu < 1) return fail(REGENVC_ERR_INVALID_ARG, "%s: n_cu=%d < 1", fn, n_cu);
+    if (D != 64 && D != 128) return fail(REGENVC_ERR_UNSUPPORTED, "%s: D=%d not in {64, 128}", fn, D);
+    regenvc::AttnPlan pl{};
+    if (!regenvc::plan_attn(B, H, Sq, Skv, D, n_cu, &pl, Skv2))
+        return fail(REGENVC_ERR_UNSUPPORTED, "%s: too many query tiles", fn);
+    plan->query_tiles = pl.n_tiles;
+    plan->key_tiles = pl.n_kt + pl.n_kt2;
+    plan->whole_tiles = pl.n_dp;
+    plan->split_tiles = pl.n_tiles - pl.n_dp;
+    plan->key_ranges = pl.n_units > 0 ? pl.seg + pl.seg2 : 0;
+    plan->workspace_bytes = (int64_t)regenvc::workspace_bytes(pl, D);
+    g_last_error[0] = '\0';
+    return REGENVC_OK;
+}
+
+}  // namespace
+
 regenvc_status regenvc_attn_plan_query(int32_t B, int32_t H, int32_t Sq, int32_t Skv, int32_t D, int32_t n_cu,
                                        regenvc_attn_plan *plan)
 {
-    if (plan == nullptr) return fail(REGENVC_ERR_INVALID_ARG, "regenvc_attn_plan_query: plan is NULL");
-    if (B < 0 || H < 0 || Sq < 0)
-        return fail(REGENVC_ERR_INVALID_ARG, "regenvc_attn_plan_query: negative size (B=%d H=%d Sq=%d)", B, H, Sq);
-    if (Skv < 1) return fail(REGENVC_ERR_INVALID_ARG, "regenvc_attn_plan_query: Skv=%d < 1", Skv);
-    if (n_cu < 1) return fail(REGENVC_ERR_INVALID_ARG, "regenvc_attn_plan_query: n_cu=%d < 1", n_cu);
-    if (D != 64 && D != 128) return fail(REGENVC_ERR_UNSUPPORTED, "regenvc_attn_plan_query: D=%d not in {64, 128}", D);
-    regenvc::AttnPlan pl{};
-    if (!regenvc::plan_attn(B, H, Sq, Skv, D, n_cu, &pl))
-        return fail(REGENVC_ERR_UNSUPPORTED, "regenvc_attn_plan_query: too many query tiles");
-    plan->query_tiles = pl.n_tiles;
-    plan->key_tiles = pl.n_kt;
-    plan->whole_tiles = pl.n_dp;
-    plan->split_tiles = pl.n_tiles - pl.n_dp;
-    plan->key_ranges = pl.n_units > 0 ? pl.seg : 0;
-    plan->workspace_bytes = (int64_t)regenvc::workspace_bytes(pl, D);
+    return plan_query("regenvc_attn_plan_query", B, H, Sq, Skv, 0, D, n_cu, plan);
+}
+
+regenvc_status regenvc_cross_attn_dual_plan_query(int32_t B, int32_t H, int32_t Sq, int32_t S_txt, int32_t S_img,
+                                                  int32_t D, int32_t n_cu, regenvc_attn_plan *plan)
+{
+    if (S_img < 1)
+        return fail(REGENVC_ERR_INVALID_ARG, "regenvc_cross_attn_dual_plan_query: S_img=%d < 1", S_img);
+    return plan_query("regenvc_cross_attn_dual_plan_query", B, H, Sq, S_txt, S_img, D, n_cu, plan);
+}
+
+regenvc_status regenvc_attn_set_workspace(void *workspace, int64_t bytes)
+{
+    if (workspace == nullptr) {
+        g_ws_ptr = nullptr;
+        g_ws_bytes = 0;
+        g_last_error[0] = '\0';
+        return REGENVC_OK;
+    }
+    if (bytes < 0) return fail(REGENVC_ERR_INVALID_ARG, "regenvc_attn_set_workspace: bytes=%lld < 0", (long long)bytes);
+    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+        return fail(REGENVC_ERR_UNSUPPORTED, "regenvc_attn_set_workspace: workspace is not 256-byte aligned");
+    g_ws_ptr = workspace;
+    g_ws_bytes = bytes;
+    g_last_error[0] = '\0';
     return REGENVC_OK;
+}
+
+int64_t regenvc_attn_pool_draws(void)
+{
+    return regenvc::pool_draws();
 }
 
 const char *regenvc_status_str(regenvc_status status)

@@ -65,6 +65,7 @@
 #include <mutex>
 #include <type_traits>
 
+
 namespace regenvc {
 namespace {
 
@@ -1647,8 +1648,11 @@ int cu_count()
     return n;
 }
 
+std::atomic<int64_t> g_pool_draws{0};
+
 // Stream-ordered workspace for split-tile partials, from a per-device pool
 // that keeps its memory (so steady-state calls do not go back to the driver).
+// Used only by calls that are not given a workspace.
 hipMemPool_t workspace_pool()
 {
     static std::mutex mu;
@@ -1683,20 +1687,27 @@ int forced_schedule()
 }
 
 template <int D, bool OUT_F32>
-hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream)
+hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream, const Workspace &given)
 {
     constexpr int BM = kWaves * 32;
     AttnPlan pl{};
     if (OUT_F32 && a.k2 != nullptr) return hipErrorInvalidValue;  // dual context: bf16 output only
     if (!plan_attn(a.B, a.H, a.Sq, a.Skv, D, cu_count(), &pl, a.k2 != nullptr ? a.Skv2 : 0))
         return hipErrorInvalidConfiguration;
-    void *ws = nullptr;
+    void *ws = nullptr;     // pool allocation to return
     if (pl.n_units > 0) {
         const size_t bytes = workspace_bytes(pl, D);
-        hipMemPool_t pool = workspace_pool();
-        hipError_t e = pool ? hipMallocFromPoolAsync(&ws, bytes, pool, stream) : hipErrorOutOfMemory;
-        if (e != hipSuccess) return e;
-        pl.ws_o = static_cast<float *>(ws);
+        void *buf = given.ptr;
+        if (buf != nullptr) {
+            if (given.bytes < bytes) return hipErrorInvalidValue;  // checked by the caller beforehand
+        } else {
+            hipMemPool_t pool = workspace_pool();
+            hipError_t e = pool ? hipMallocFromPoolAsync(&ws, bytes, pool, stream) : hipErrorOutOfMemory;
+            if (e != hipSuccess) return e;
+            g_pool_draws.fetch_add(1);
+            buf = ws;
+        }
+        pl.ws_o = static_cast<float *>(buf);
         pl.ws_lse = pl.ws_o + (size_t)pl.n_units * BM * D;
     }
     const dim3 grid((unsigned)(pl.n_dp + pl.n_units)), block(kThreads);
@@ -1754,10 +1765,29 @@ size_t workspace_bytes(const AttnPlan &pl, int D)
     return (size_t)pl.n_units * (kWaves * 32) * (D + 1) * sizeof(float);
 }
 
-hipError_t launch_attn(const AttnArgs &a, hipStream_t stream)
+int device_cu_count()
 {
-    if (a.D == 128) return a.o_f32 ? launch_attn_t<128, true>(a, stream) : launch_attn_t<128, false>(a, stream);
-    if (a.D == 64) return a.o_f32 ? launch_attn_t<64, true>(a, stream) : launch_attn_t<64, false>(a, stream);
+    return cu_count();
+}
+
+size_t attn_workspace_need(const AttnArgs &a)
+{
+    AttnPlan pl{};
+    if (!plan_attn(a.B, a.H, a.Sq, a.Skv, a.D, cu_count(), &pl, a.k2 != nullptr ? a.Skv2 : 0)) return 0;
+    return workspace_bytes(pl, a.D);
+}
+
+int64_t pool_draws()
+{
+    return g_pool_draws.load();
+}
+
+hipError_t launch_attn(const AttnArgs &a, hipStream_t stream, const Workspace &ws)
+{
+    if (a.D == 128)
+        return a.o_f32 ? launch_attn_t<128, true>(a, stream, ws) : launch_attn_t<128, false>(a, stream, ws);
+    if (a.D == 64)
+        return a.o_f32 ? launch_attn_t<64, true>(a, stream, ws) : launch_attn_t<64, false>(a, stream, ws);
     return hipErrorInvalidValue;
 }
 

@@ -100,8 +100,21 @@ struct NormRopeArgs {
 bool plan_attn(int B, int H, int Sq, int Skv, int D, int n_cu, AttnPlan *out, int Skv2 = 0);
 // Bytes of split-tile partials a plan needs (0 when nothing is split).
 size_t workspace_bytes(const AttnPlan &pl, int D);
+// Compute units of the current device (cached per device).
+int device_cu_count();
+// Bytes of split-tile partials the launch `a` needs on the current device.
+size_t attn_workspace_need(const AttnArgs &a);
 
-hipError_t launch_attn(const AttnArgs &a, hipStream_t stream);
+// Where an attention launch takes its split-tile partials from: stream-ordered
+// from the library's per-device pool, or a caller-given buffer of at least
+// attn_workspace_need() bytes (no allocation then).
+struct Workspace {
+    void *ptr = nullptr;  // null: the pool
+    size_t bytes = 0;
+};
+hipError_t launch_attn(const AttnArgs &a, hipStream_t stream, const Workspace &ws);
+// Number of launches so far (all devices) that drew their partials from the pool.
+int64_t pool_draws();
 hipError_t launch_merge(const MergeArgs &a, hipStream_t stream);
 hipError_t launch_empty_partial(const FillArgs &a, hipStream_t stream);
 hipError_t launch_norm_rope(const NormRopeArgs &a, hipStream_t stream);

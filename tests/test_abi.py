@@ -22,13 +22,14 @@ def lib():
 
 def declared_functions():
     text = open(HEADER).read()
-    return sorted(set(re.findall(r"^\s*(?:regenvc_status|const char \*)\s*(regenvc_\w+)\s*\(", text, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:regenvc_status|const char \*|int64_t)\s*(regenvc_\w+)\s*\(", text, re.M)))
 
 
 def test_header_declares_the_entry_points():
     names = declared_functions()
     for n in ["regenvc_attn_fwd", "regenvc_attn_partial_fwd", "regenvc_lse_merge", "regenvc_cross_attn_fwd",
-              "regenvc_status_str", "regenvc_last_error"]:
+              "regenvc_status_str", "regenvc_last_error", "regenvc_attn_set_workspace",
+              "regenvc_cross_attn_dual_plan_query", "regenvc_attn_pool_draws"]:
         assert n in names
 
 
@@ -244,3 +245,38 @@ def test_cross_attn_dual_validation(lib):
 @pytest.mark.skipif(has_gpu_node(), reason="would reach a launch on fake addresses on a GPU machine")
 def test_cross_attn_dual_valid_arguments_reach_the_device_check(lib):
     expect(lib, dual(lib, lt=FAKE + 0x4000000, li=FAKE + 0x4100000), _lib.ERR_HIP, "hip")
+
+
+def test_workspace_binding_validation(lib):
+    """regenvc_attn_set_workspace is host-only: alignment and size are checked
+    on the spot; NULL unbinds."""
+    expect(lib, lib.regenvc_attn_set_workspace(FAKE + 16, 4096), _lib.ERR_UNSUPPORTED, "256-byte")
+    expect(lib, lib.regenvc_attn_set_workspace(FAKE, -1), _lib.ERR_INVALID_ARG, "bytes")
+    expect(lib, lib.regenvc_attn_set_workspace(FAKE, 1 << 20), _lib.OK)
+    # a bound workspace leaves argument validation as it was (still before any HIP call)
+    expect(lib, attn(lib, D=96), _lib.ERR_UNSUPPORTED, "head dim")
+    expect(lib, lib.regenvc_attn_set_workspace(None, 0), _lib.OK)
+    expect(lib, lib.regenvc_attn_set_workspace(None, -5), _lib.OK)  # bytes ignored when unbinding
+
+
+def test_dual_plan_query(lib):
+    """The dual cross-attention plan at the window shape (10920 queries, 12
+    heads, 512 + 257 context tokens): 516 query tiles, 8 + 5 key tiles, two
+    whole rounds on 256 CUs and the 4 leftover tiles split over both
+    contexts; workspace = ranges x 256 rows x (D + 1) floats."""
+    plan = _lib.AttnPlan()
+    expect(lib, lib.regenvc_cross_attn_dual_plan_query(1, 12, 10920, 512, 257, 128, 256, ctypes.byref(plan)),
+           _lib.OK)
+    assert plan.query_tiles == 516 and plan.key_tiles == 13
+    assert plan.whole_tiles == 512 and plan.split_tiles == 4 and plan.key_ranges >= 2
+    assert plan.workspace_bytes == plan.split_tiles * plan.key_ranges * 256 * 129 * 4
+    expect(lib, lib.regenvc_cross_attn_dual_plan_query(1, 12, 10920, 512, 0, 128, 256, ctypes.byref(plan)),
+           _lib.ERR_INVALID_ARG, "S_img")
+    expect(lib, lib.regenvc_cross_attn_dual_plan_query(1, 12, 10920, 0, 257, 128, 256, ctypes.byref(plan)),
+           _lib.ERR_INVALID_ARG, "key count")
+    expect(lib, lib.regenvc_cross_attn_dual_plan_query(1, 12, 10920, 512, 257, 96, 256, ctypes.byref(plan)),
+           _lib.ERR_UNSUPPORTED, "D=96")
+
+
+def test_pool_draws_is_host_only(lib):
+    assert lib.regenvc_attn_pool_draws() >= 0
