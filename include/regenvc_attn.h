@@ -66,6 +66,7 @@
 #ifndef REGENVC_ATTN_H
 #define REGENVC_ATTN_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -112,6 +113,27 @@ regenvc_status regenvc_attn_fwd(const regenvc_tensor *q, const regenvc_tensor *k
                                 regenvc_dtype o_dtype, float *lse,
                                 int32_t B, int32_t H, int32_t Sq, int32_t Skv,
                                 int32_t D, float softmax_scale, void *stream);
+
+/* The same call as regenvc_attn_fwd (same arguments, rules and results,
+   bitwise) for callers that cannot allocate: code under HIP graph capture,
+   tight serving loops, harnesses that forbid hipMalloc.  It allocates
+   nothing and ignores any regenvc_attn_set_workspace binding: the split-tile
+   partials go to a static device array of REGENVC_NOALLOC_SCRATCH_BYTES
+   inside the library, one copy per GPU, which each GPU the library runs on
+   holds until the process ends (its address is looked up once per device,
+   at the first call there).  A call whose plan needs more scratch than that
+   (workspace_bytes of regenvc_attn_plan_query) returns
+   REGENVC_ERR_UNSUPPORTED and enqueues nothing.  Every call on a GPU shares
+   that GPU's array, which keeps the last call's contents (nothing in it has
+   to start at zero): calls that overlap in time on one GPU -- on different
+   streams, or from different threads without ordering -- race on it, so
+   order them (one stream, or synchronize). */
+#define REGENVC_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+regenvc_status regenvc_attn_fwd_noalloc(const regenvc_tensor *q, const regenvc_tensor *k,
+                                        const regenvc_tensor *v, const regenvc_tensor *o,
+                                        regenvc_dtype o_dtype, float *lse,
+                                        int32_t B, int32_t H, int32_t Sq, int32_t Skv,
+                                        int32_t D, float softmax_scale, void *stream);
 
 /* Partial attention of every query over ONE key/value chunk (Sec. 3.5,
    Ring: key/value blocks are passed around and folded together with

@@ -36,6 +36,8 @@ _FP = ctypes.POINTER(ctypes.c_float)
 _SIGNATURES = {
     "regenvc_attn_fwd": [_PT, _PT, _PT, _PT, ctypes.c_int, ctypes.c_void_p,
                          _i32, _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_void_p],
+    "regenvc_attn_fwd_noalloc": [_PT, _PT, _PT, _PT, ctypes.c_int, ctypes.c_void_p,
+                                 _i32, _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_void_p],
     "regenvc_attn_partial_fwd": [_PT, _PT, _PT, _PT, ctypes.c_void_p,
                                  _i32, _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_void_p],
     "regenvc_lse_merge": [ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(ctypes.c_void_p), _i32,

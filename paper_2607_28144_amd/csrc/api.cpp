@@ -169,11 +169,13 @@ struct Ctx2 {
 // run_o (ring accumulate only): f32 running output, read; lse is then the
 // running LSE, read and rewritten in place; o may be run_o itself (f32).
 // ctx2 (dual cross-attention only): the second context, summed into o.
+// no_alloc: split-tile partials in the library's static device scratch
+// (regenvc_attn_fwd_noalloc) instead of a bound workspace or the pool.
 regenvc_status attn_common(const char *fn, const regenvc_tensor *q, const regenvc_tensor *k,
                            const regenvc_tensor *v, const regenvc_tensor *o, regenvc_dtype o_dtype, float *lse,
                            bool lse_required, int32_t B, int32_t H, int32_t Sq, int32_t Skv, int32_t D, float scale,
                            void *stream, bool allow_empty_keys, const regenvc_tensor *run_o = nullptr,
-                           const Ctx2 *ctx2 = nullptr)
+                           const Ctx2 *ctx2 = nullptr, bool no_alloc = false)
 {
     regenvc_status st = check_sizes(B, H, Sq, D);
     if (st != REGENVC_OK) return st;
@@ -295,9 +297,22 @@ regenvc_status attn_common(const char *fn, const regenvc_tensor *q, const regenv
         a.run_lse = lse;
         a.r_sb = run_o->stride_b, a.r_ss = run_o->stride_s, a.r_sh = run_o->stride_h;
     }
-    // split-tile partials: the workspace bound on this thread, else the pool
+    // split-tile partials: the static scratch (no_alloc), the workspace bound
+    // on this thread, else the pool
     regenvc::Workspace ws{};
-    if (g_ws_ptr != nullptr) {
+    if (no_alloc) {
+        const size_t need = regenvc::attn_workspace_need(a);
+        if (need > regenvc::kNoAllocScratchBytes)
+            return fail(REGENVC_ERR_UNSUPPORTED,
+                        "%s: this call needs %zu bytes of scratch, more than the %zu bytes the no-allocation entry "
+                        "point holds",
+                        fn, need, regenvc::kNoAllocScratchBytes);
+        void *p = nullptr;
+        const hipError_t e = regenvc::noalloc_scratch(&p);
+        if (e != hipSuccess) return fail(REGENVC_ERR_HIP, "%s: scratch lookup: %s", fn, hipGetErrorString(e));
+        ws.ptr = p;
+        ws.bytes = regenvc::kNoAllocScratchBytes;
+    } else if (g_ws_ptr != nullptr) {
         const size_t need = regenvc::attn_workspace_need(a);
         if ((size_t)g_ws_bytes < need)
             return fail(REGENVC_ERR_INVALID_ARG, "%s: the bound workspace holds %lld bytes, this call needs %zu", fn,
@@ -327,6 +342,16 @@ regenvc_status regenvc_attn_fwd(const regenvc_tensor *q, const regenvc_tensor *k
 {
     return attn_common("regenvc_attn_fwd", q, k, v, o, o_dtype, lse, false, B, H, Sq, Skv, D, softmax_scale, stream,
                        false);
+}
+
+regenvc_status regenvc_attn_fwd_noalloc(const regenvc_tensor *q, const regenvc_tensor *k, const regenvc_tensor *v,
+                                        const regenvc_tensor *o, regenvc_dtype o_dtype, float *lse, int32_t B,
+                                        int32_t H, int32_t Sq, int32_t Skv, int32_t D, float softmax_scale,
+                                        void *stream)
+{
+    static_assert(REGENVC_NOALLOC_SCRATCH_BYTES == regenvc::kNoAllocScratchBytes, "header and library agree");
+    return attn_common("regenvc_attn_fwd_noalloc", q, k, v, o, o_dtype, lse, false, B, H, Sq, Skv, D, softmax_scale,
+                       stream, false, nullptr, nullptr, true);
 }
 
 regenvc_status regenvc_attn_partial_fwd(const regenvc_tensor *q, const regenvc_tensor *k_chunk,

@@ -65,6 +65,10 @@
 #include <mutex>
 #include <type_traits>
 
+// Split-tile partials of regenvc_attn_fwd_noalloc (callers that cannot
+// allocate).  In host code this name is only a stand-in for the symbol:
+// kernels get the device address from regenvc::noalloc_scratch().
+static __device__ __align__(256) char scratch[regenvc::kNoAllocScratchBytes];
 
 namespace regenvc {
 namespace {
@@ -1780,6 +1784,27 @@ size_t attn_workspace_need(const AttnArgs &a)
 int64_t pool_draws()
 {
     return g_pool_draws.load();
+}
+
+hipError_t noalloc_scratch(void **out)
+{
+    static std::mutex mu;
+    static void *addr[64] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (addr[dev] == nullptr) {
+        // once per device, with that device current: each GPU holds its own copy
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        addr[dev] = p;
+    }
+    *out = addr[dev];
+    return hipSuccess;
 }
 
 hipError_t launch_attn(const AttnArgs &a, hipStream_t stream, const Workspace &ws)

@@ -115,6 +115,13 @@ struct Workspace {
 hipError_t launch_attn(const AttnArgs &a, hipStream_t stream, const Workspace &ws);
 // Number of launches so far (all devices) that drew their partials from the pool.
 int64_t pool_draws();
+
+// Scratch of the no-allocation entry point: a file-scope static device array
+// of kNoAllocScratchBytes, one copy per GPU (held until the process ends).
+// noalloc_scratch() gives its device address on the current device, looked
+// up with hipGetSymbolAddress once per device and kept.
+constexpr size_t kNoAllocScratchBytes = (size_t)32 << 20;
+hipError_t noalloc_scratch(void **ptr);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t stream);
 hipError_t launch_empty_partial(const FillArgs &a, hipStream_t stream);
 hipError_t launch_norm_rope(const NormRopeArgs &a, hipStream_t stream);
