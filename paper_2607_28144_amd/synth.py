@@ -57,3 +57,50 @@ def qkv(seed: int, B: int, H: int, Sq: int, Skv: int, D: int, ctx: int = 0):
 def default_scale(D: int) -> float:
     """1/sqrt(D) rounded to float32 (the value both sides receive)."""
     return float(np.float32(1.0 / np.sqrt(D)))
+
+
+# Parameters of one diffusion-transformer block (model width 1536 = 12 heads
+# x 128, feed-forward 8960, six adaLN vectors): name -> shape; linear-layer
+# weights are [out, in].
+DIT_WIDTH, DIT_HEADS, DIT_FFN = 1536, 12, 8960
+DIT_PARAM_SHAPES = {
+    "w_mod": (6 * DIT_WIDTH, DIT_WIDTH), "b_mod": (6 * DIT_WIDTH,),
+    "w_qkv": (3 * DIT_WIDTH, DIT_WIDTH), "b_qkv": (3 * DIT_WIDTH,), "w_qn": (DIT_WIDTH,), "w_kn": (DIT_WIDTH,),
+    "w_o": (DIT_WIDTH, DIT_WIDTH), "b_o": (DIT_WIDTH,),
+    "w_n3": (DIT_WIDTH,), "b_n3": (DIT_WIDTH,),
+    "w_qc": (DIT_WIDTH, DIT_WIDTH), "b_qc": (DIT_WIDTH,), "w_qcn": (DIT_WIDTH,),
+    "w_oc": (DIT_WIDTH, DIT_WIDTH), "b_oc": (DIT_WIDTH,),
+    "w_1": (DIT_FFN, DIT_WIDTH), "b_1": (DIT_FFN,),
+    "w_2": (DIT_WIDTH, DIT_FFN), "b_2": (DIT_WIDTH,),
+}
+# per-channel scales of the normalizations: 1 + N(0, 0.02^2) (not N(0, 0.02),
+# which would zero the signal); every other parameter N(0, 0.02^2)
+DIT_NORM_SCALES = ("w_qn", "w_kn", "w_n3", "w_qcn")
+
+
+def dit_params(seed: int) -> dict:
+    """Synthetic bf16 parameters of one block (bits), in DIT_PARAM_SHAPES
+    order from np.random.default_rng(seed): weights and biases N(0, 0.02^2),
+    normalization scales 1 + N(0, 0.02^2) (trained weights are not
+    available)."""
+    rng = np.random.default_rng(seed)
+    out = {}
+    for name, shape in DIT_PARAM_SHAPES.items():
+        x = rng.standard_normal(size=shape, dtype=np.float32) * np.float32(0.02)
+        if name in DIT_NORM_SCALES:
+            x = x + np.float32(1.0)
+        out[name] = f32_to_bf16_bits(x)
+    return out
+
+
+def dit_inputs(seed: int, S: int, S_ctx: int, steps: int = 4):
+    """Block inputs: residual stream x float32 [S, 1536] ~ N(0, 1); one
+    conditioning vector per denoising step, float32 [steps, 1536] ~ N(0, 1)
+    (standing in for the timestep embeddings of the four-step schedule); and
+    the context's precomputed key/values, bf16 bits [S_ctx, 12, 128] ~ N(0, 1)."""
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal(size=(S, DIT_WIDTH), dtype=np.float32)
+    e = rng.standard_normal(size=(steps, DIT_WIDTH), dtype=np.float32)
+    kc = normal_bf16(rng, (S_ctx, DIT_HEADS, DIT_WIDTH // DIT_HEADS))
+    vc = normal_bf16(rng, (S_ctx, DIT_HEADS, DIT_WIDTH // DIT_HEADS))
+    return x, e, kc, vc
