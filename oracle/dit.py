@@ -126,13 +126,16 @@ def _attention(q: np.ndarray, k_bits: np.ndarray, v_bits: np.ndarray) -> np.ndar
 
 
 def block(x: np.ndarray, e: np.ndarray, p: dict, ctx_k: np.ndarray, ctx_v: np.ndarray, grid,
-          token0: int = 0, theta: float = 10000.0) -> np.ndarray:
+          token0: int = 0, theta: float = 10000.0, rows=None) -> np.ndarray:
     """One forward of the block.  x: float64 [S, C] residual stream (tokens in
     (frame, row, column) raster order on `grid`); e: [C] conditioning vector;
     p: the block's parameters as bf16 bits (w_* of linear layers [out, in]);
-    ctx_k, ctx_v:
-    the context's key/values, bf16 bits [Sctx, H, D].  Returns the new x."""
+    ctx_k, ctx_v: the context's key/values, bf16 bits [Sctx, H, D].  Returns
+    the new x; with `rows` (indices), only those rows of it -- every step but
+    the self-attention's keys and values is row by row, and those still come
+    from all S rows."""
     x = np.array(x, dtype=np.float64)
+    sel = np.arange(x.shape[0]) if rows is None else np.asarray(rows)
     S = x.shape[0]
     W = {n: widen(v) for n, v in p.items()}
     sh1, sc1, g1, sh2, sc2, g2 = modulation(e, W["w_mod"], W["b_mod"])
@@ -143,8 +146,8 @@ def block(x: np.ndarray, e: np.ndarray, p: dict, ctx_k: np.ndarray, ctx_v: np.nd
     q, k, v = qkv[:, :C], qkv[:, C:2 * C], qkv[:, 2 * C:]
     qr = round_bf16(_norm_rope(to_bits(q).reshape(1, S, HEADS, HEAD_DIM), p["w_qn"], grid, token0, EPS, theta))
     kr = round_bf16(_norm_rope(to_bits(k).reshape(1, S, HEADS, HEAD_DIM), p["w_kn"], grid, token0, EPS, theta))
-    a = _attention(qr.reshape(S, C), to_bits(kr), to_bits(v))
-    x = x + g1 * gemm(a, W["w_o"], W["b_o"])
+    a = _attention(qr.reshape(S, C)[sel], to_bits(kr), to_bits(v))
+    x = x[sel] + g1 * gemm(a, W["w_o"], W["b_o"])
 
     # cross-attention branch
     h2 = round_bf16(layer_norm(x, EPS, W["w_n3"], W["b_n3"]))

@@ -24,6 +24,15 @@ class AttnPlan(ctypes.Structure):
                 ("key_ranges", ctypes.c_int32), ("workspace_bytes", ctypes.c_int64)]
 
 
+DIT_PARAM_NAMES = ("w_mod", "b_mod", "w_qkv", "b_qkv", "w_qn", "w_kn", "w_o", "b_o", "w_n3", "b_n3", "w_qc",
+                   "b_qc", "w_qcn", "w_oc", "b_oc", "w_1", "b_1", "w_2", "b_2")
+
+
+class DitParams(ctypes.Structure):
+    """regenvc_dit_params: device pointers of one block's bf16 parameters."""
+    _fields_ = [(n, ctypes.c_void_p) for n in DIT_PARAM_NAMES]
+
+
 class RegenvcError(RuntimeError):
     def __init__(self, status: int, fn: str, detail: str):
         self.status = status
@@ -51,6 +60,19 @@ _SIGNATURES = {
     "regenvc_attn_plan_query": [_i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(AttnPlan)],
     "regenvc_cross_attn_dual_plan_query": [_i32, _i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(AttnPlan)],
     "regenvc_attn_set_workspace": [ctypes.c_void_p, ctypes.c_int64],
+    "regenvc_linear_fwd": [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                           ctypes.c_void_p, ctypes.c_int64, _i32, _i32, _i32, _i32, ctypes.c_void_p],
+    "regenvc_layer_norm_fwd": [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, _i32, _i32, ctypes.c_float,
+                               ctypes.c_void_p],
+    "regenvc_rms_norm_fwd": [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                             _i32, _i32, ctypes.c_float, ctypes.c_void_p],
+    "regenvc_dit_modulation": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, _i32, _i32,
+                               ctypes.c_void_p],
+    "regenvc_dit_block_workspace": [_i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_int64)],
+    "regenvc_dit_block_fwd": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                              _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, ctypes.c_void_p,
+                              ctypes.c_int64, ctypes.c_void_p],
     "regenvc_qk_norm_rope": [_PT, _PT, ctypes.c_void_p, ctypes.c_void_p, _PT, _PT, _i32, _i32, _i32, _i32,
                              _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_float, ctypes.c_void_p],
 }

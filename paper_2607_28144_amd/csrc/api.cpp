@@ -608,3 +608,30 @@ const char *regenvc_last_error(void)
 }
 
 }  // extern "C"
+
+// Status helpers shared with the other entry-point files (abi_util.hpp).
+namespace regenvc {
+namespace abi {
+
+regenvc_status fail_msg(regenvc_status st, const char *msg)
+{
+    return fail(st, "%s", msg);
+}
+
+regenvc_status device_ok()
+{
+    return check_device();
+}
+
+regenvc_status launch_status(hipError_t e, const char *what)
+{
+    return launched(e, what);
+}
+
+void clear_error()
+{
+    g_last_error[0] = '\0';
+}
+
+}  // namespace abi
+}  // namespace regenvc

@@ -21,7 +21,7 @@ def lib():
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    text = open(HEADER).read() + open(os.path.join(REPO, "include", "regenvc_dit.h")).read()
     return sorted(set(re.findall(r"^\s*(?:regenvc_status|const char \*|int64_t)\s*(regenvc_\w+)\s*\(", text, re.M)))
 
 

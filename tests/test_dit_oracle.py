@@ -278,3 +278,13 @@ def test_planted_mistakes_are_caught(name, old, new, params):
             return False
     results = [holds(p) for p in ELEMENTWISE_PINS] + [holds(p, params) for p in BLOCK_PINS]
     assert not all(results), f"mutant '{name}' passes every pin"
+
+
+def test_row_subset_equals_the_rows_of_the_full_block(params):
+    """The rows option restricts the output, not the keys: block(rows=r) is
+    block()[r] (a check of the option, not a pin of the definition)."""
+    x, e, kc, vc = synth.dit_inputs(13, 2 * 3 * 4, 7, steps=1)
+    full = dit.block(x.astype(np.float64), e[0], params, kc, vc, (2, 3, 4))
+    rows = [0, 5, 17, 23]
+    sub = dit.block(x.astype(np.float64), e[0], params, kc, vc, (2, 3, 4), rows=rows)
+    assert np.array_equal(sub, full[rows])

@@ -1,0 +1,227 @@
+"""GPU parity of the diffusion-transformer block kernels and of the block
+forward (include/regenvc_dit.h) against the fp64 block oracle (oracle/dit.py)
+on the same seeded bf16 inputs.
+
+Per-kernel bounds follow from the arithmetic: the kernels accumulate in fp32
+(error well below 2^-20 of sum |a_k w_k| for these K) and round bf16 outputs
+once (at most 2^-8 of the value), so a bf16 output must satisfy
+|gpu - ref| <= 2^-8 |ref| + 2 * 2^-20 * sum_k |a_k||w_k| (plus a GELU slope
+of at most 1.13, and 1e-6 for the fp32 exponential); float32 outputs
+(gated residual, modulation vectors) carry only the accumulation term and
+float32 rounding.
+
+The composed block differs from the oracle through bf16 rounding flips: a
+value whose fp32 and fp64 forms straddle a bf16 rounding boundary is stored
+one bf16 step apart, and the following layers carry the step on (the
+attention's bf16 weights and the 8960-deep feed-forward sum many of them).
+How far two correct bf16 implementations drift apart this way is measured,
+not guessed: the tests run the oracle a second time with every value
+perturbed by 1e-5 (relative, seeded) just before each bf16 rounding -- any
+perturbation that small gives the same spread, about 1.1e-3 relative RMS
+after one step and 2e-3 after four -- and hold the GPU to twice that
+spread per step in relative RMS and in max error (relative to max|x|).  A
+dropped 0.02 bias in any branch moves the stream by ~9e-3 of its RMS.
+"""
+import numpy as np
+import pytest
+
+from oracle import dit as odit
+from paper_2607_28144_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+ULP = 2.0 ** -8
+ACC = 2.0 ** -20
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_28144_amd import dit  # noqa: F401  (fails loudly if the library is missing)
+    yield
+    torch.cuda.synchronize()
+
+
+def kern():
+    from paper_2607_28144_amd import dit
+    return dit
+
+
+def dev_bits(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def host(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def check_bound(name, got, ref, tol):
+    err = np.abs(got - ref)
+    ratio = float((err / tol).max())
+    over = int(np.count_nonzero(err > tol))
+    print(f"[dit] {name}: max|d|={err.max():.3e} rms={np.sqrt((err * err).mean()):.3e} "
+          f"max err/bound={ratio:.3f} over={over}/{err.size}", flush=True)
+    assert np.all(np.isfinite(got)), f"{name}: non-finite output"
+    assert over == 0, f"{name}: {over} elements over the bound (worst err/bound {ratio:.3f})"
+
+
+def bits(rng, shape, scale=1.0):
+    return synth.normal_bf16(rng, shape, scale)
+
+
+@pytest.mark.parametrize("M,N,K", [(300, 256, 1536), (1000, 1536, 1536), (577, 4608, 1536), (333, 1536, 8960),
+                                   (10920, 1536, 1536)])
+def test_linear_epilogues(M, N, K):
+    rng = np.random.default_rng(M + N + K)
+    a, w, b = bits(rng, (M, K)), bits(rng, (N, K), 0.02), bits(rng, (N,), 0.02)
+    gate = rng.standard_normal(N).astype(np.float32)
+    x0 = rng.standard_normal((M, N)).astype(np.float32)
+    A, Wt, B = odit.widen(a), odit.widen(w), odit.widen(b)
+    y = odit.gemm(A, Wt, B)
+    slack = 2 * ACC * (np.abs(A) @ np.abs(Wt).T)
+    da, dw, db = dev_bits(a), dev_bits(w), dev_bits(b)
+    out = kern().linear_fwd(da, dw, db, "bias")
+    out_g = kern().linear_fwd(da, dw, db, "bias_gelu")
+    xr = torch.from_numpy(x0).cuda()
+    kern().linear_fwd(da, dw, db, "gated_residual", gate=torch.from_numpy(gate).cuda(), out=xr)
+    torch.cuda.synchronize()
+    check_bound(f"linear bias M={M} N={N} K={K}", host(out), y, ULP * np.abs(y) + slack)
+    g = odit.gelu_tanh(y)
+    check_bound(f"linear bias+gelu M={M} N={N} K={K}", host(out_g), g, ULP * np.abs(g) + 1.13 * slack + 1e-6)
+    xref = x0.astype(np.float64) + gate.astype(np.float64) * y
+    check_bound(f"linear gated residual M={M} N={N} K={K}", host(xr), xref,
+                np.abs(gate) * slack + 2.0 ** -22 * (np.abs(x0) + np.abs(gate * y)) + 1e-7)
+
+
+def test_linear_without_bias_or_gate_into_a_strided_output():
+    """No bias, no gate (1), the output a column slice of a wider buffer."""
+    rng = np.random.default_rng(5)
+    M, N, K = 400, 512, 1536
+    a, w = bits(rng, (M, K)), bits(rng, (N, K), 0.02)
+    wide = torch.zeros((M, N + 256), dtype=torch.float32, device="cuda")
+    kern().linear_fwd(dev_bits(a), dev_bits(w), None, "gated_residual", out=wide[:, 128:128 + N])
+    torch.cuda.synchronize()
+    y = odit.gemm(odit.widen(a), odit.widen(w))
+    slack = 2 * ACC * (np.abs(odit.widen(a)) @ np.abs(odit.widen(w)).T)
+    got = host(wide)
+    check_bound("linear plain into a column slice", got[:, 128:128 + N], y, slack + 1e-7)
+    assert np.all(got[:, :128] == 0) and np.all(got[:, 128 + N:] == 0)
+
+
+def test_layer_norm_both_forms():
+    rng = np.random.default_rng(6)
+    rows, C = 777, 1536
+    x = (rng.standard_normal((rows, C)) * 3 + 0.5).astype(np.float32)
+    shift, scale = rng.standard_normal(C).astype(np.float32), rng.standard_normal(C).astype(np.float32)
+    w, b = bits(rng, (C,)), bits(rng, (C,))
+    dx = torch.from_numpy(x).cuda()
+    y1 = kern().layer_norm_fwd(dx, shift=torch.from_numpy(shift).cuda(), scale=torch.from_numpy(scale).cuda())
+    y2 = kern().layer_norm_fwd(dx, w=dev_bits(w), b=dev_bits(b))
+    torch.cuda.synchronize()
+    ln = odit.layer_norm(x.astype(np.float64))
+    r1 = odit.modulate(ln, shift.astype(np.float64), scale.astype(np.float64))
+    r2 = ln * odit.widen(w) + odit.widen(b)
+    check_bound("layer norm, modulated", host(y1), r1, ULP * np.abs(r1) + 1e-5 * (1 + np.abs(ln) * (1 + np.abs(scale))))
+    check_bound("layer norm, affine", host(y2), r2, ULP * np.abs(r2) + 1e-5 * (1 + np.abs(ln * odit.widen(w))))
+
+
+def test_rms_norm_in_place():
+    rng = np.random.default_rng(7)
+    rows, C = 555, 1536
+    x, w = bits(rng, (rows, C), 2.0), synth.f32_to_bf16_bits(1 + 0.1 * rng.standard_normal(C).astype(np.float32))
+    dx = dev_bits(x)
+    kern().rms_norm_fwd(dx, dev_bits(w), out=dx)
+    torch.cuda.synchronize()
+    ref = odit.rms_norm(odit.widen(x), odit.widen(w))
+    check_bound("rms norm in place", host(dx), ref, ULP * np.abs(ref) + 1e-5 * (1 + np.abs(ref)))
+
+
+def test_modulation_vectors():
+    rng = np.random.default_rng(8)
+    C = 1536
+    w, b = bits(rng, (6 * C, C), 0.02), bits(rng, (6 * C,), 0.02)
+    e = rng.standard_normal(C).astype(np.float32)
+    out = kern().modulation(dev_bits(w).view(6 * C, C), dev_bits(b), torch.from_numpy(e).cuda())
+    torch.cuda.synchronize()
+    ref = odit.modulation(e.astype(np.float64), odit.widen(w), odit.widen(b)).reshape(-1)
+    s = odit.silu(e.astype(np.float64))
+    check_bound("adaLN modulation", out.cpu().numpy().astype(np.float64), ref,
+                2 * ACC * (np.abs(odit.widen(w)) @ np.abs(s)) + 1e-7)
+
+
+# ------------------------------------------------------------------ the block
+def device_block(params):
+    return kern().DitBlock({n: dev_bits(v) for n, v in params.items()})
+
+
+def rel_errors(got, ref):
+    d = got - ref
+    return float(np.sqrt((d * d).mean() / (ref * ref).mean())), float(np.abs(d).max() / np.abs(ref).max())
+
+
+def jittered_oracle(seed: int, rel: float = 1e-5):
+    """A copy of the block oracle whose every bf16 storage point rounds the
+    value times (1 + rel * N(0, 1)): a second correct bf16 implementation,
+    differing from the first only in last bits before each rounding."""
+    import types
+    src = open(odit.__file__).read()
+    mod = types.ModuleType("oracle._dit_jittered")
+    mod.__package__ = "oracle"
+    mod.__file__ = odit.__file__
+    exec(compile(src, odit.__file__ + " (jittered)", "exec"), mod.__dict__)
+    rng = np.random.default_rng(seed)
+    exact = mod.round_bf16
+    mod.round_bf16 = lambda x: exact(np.asarray(x) * (1.0 + rel * rng.standard_normal(np.shape(x))))
+    return mod
+
+
+def block_errors(name, got, ref, ref2):
+    """GPU vs oracle, held to twice the oracle's own spread (ref2: the
+    jittered oracle)."""
+    rms, mx = rel_errors(got, ref)
+    rms2, mx2 = rel_errors(ref2, ref)
+    print(f"[dit] {name}: max|dx|={np.abs(got - ref).max():.3e} (max|x|={np.abs(ref).max():.3e}) "
+          f"rms|dx|/rms|x|={rms:.3e} max|dx|/max|x|={mx:.3e}; bf16 spread of the oracle: rms {rms2:.3e} "
+          f"max {mx2:.3e}", flush=True)
+    assert np.all(np.isfinite(got))
+    assert rms <= 2 * rms2 and mx <= 2 * mx2 + 1e-4, name
+
+
+def test_block_four_steps_every_row():
+    """A 7 x 6 x 8 latent window (336 tokens), 12 heads x 128, 64 context
+    tokens, four denoising steps: every row of the residual stream."""
+    params = synth.dit_params(11)
+    x, e, kc, vc = synth.dit_inputs(12, 7 * 6 * 8, 64)
+    blk = device_block(params)
+    dx = torch.from_numpy(x).cuda()
+    dk, dv = dev_bits(kc), dev_bits(vc)
+    ref = x.astype(np.float64)
+    ref2 = ref.copy()
+    jit = jittered_oracle(1)
+    for s in range(4):
+        blk.forward(dx, torch.from_numpy(e[s]).cuda(), dk, dv, (7, 6, 8))
+        ref = odit.block(ref, e[s], params, kc, vc, (7, 6, 8))
+        ref2 = jit.block(ref2, e[s], params, kc, vc, (7, 6, 8))
+        torch.cuda.synchronize()
+        block_errors(f"block step {s + 1}, 336 tokens", dx.cpu().numpy().astype(np.float64), ref, ref2)
+
+
+def test_block_window_shape_one_step_sampled_rows():
+    """The workload's window: 10920 tokens (7 x 30 x 52), 12 heads x 128,
+    512 context tokens, one step; sampled rows of the residual stream against
+    the oracle (whose self-attention still sees every key)."""
+    params = synth.dit_params(21)
+    S = 7 * 30 * 52
+    x, e, kc, vc = synth.dit_inputs(22, S, 512, steps=1)
+    blk = device_block(params)
+    dx = torch.from_numpy(x).cuda()
+    blk.forward(dx, torch.from_numpy(e[0]).cuda(), dev_bits(kc), dev_bits(vc), (7, 30, 52))
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, 1, 255, 256, 1559, 1560, S // 2, S - 2, S - 1],
+                                     np.random.default_rng(23).choice(S, 64, replace=False)]))
+    ref = odit.block(x.astype(np.float64), e[0], params, kc, vc, (7, 30, 52), rows=rows)
+    ref2 = jittered_oracle(2).block(x.astype(np.float64), e[0], params, kc, vc, (7, 30, 52), rows=rows)
+    block_errors("block window one step (sampled rows)", dx.cpu().numpy().astype(np.float64)[rows], ref, ref2)
