@@ -300,12 +300,72 @@ def next_steps_timing(torch, api, synth, dev, to_dev, q, kc, vc, rq, rk, rv, sca
     return {name: {"ms": min(ms[name]), "gflop": g, "tflops": g / min(ms[name])} for name, _, g in cases}
 
 
+DIT = dict(S=10920, grid=(7, 30, 52), C=1536, heads=12, F=8960, ctx=512, steps=4, seed_params=31, seed_inputs=32)
+
+
+def dit_block_leg(torch, dev, reps, warmup):
+    """The diffusion-transformer block at the window shape (10920 tokens, 12
+    heads x 128, FFN 8960, 512 context tokens) for 4 denoising steps
+    (regenvc_dit_block_fwd per step), then each of its linear layers alone
+    (regenvc_linear_fwd at the block's shapes; torch.matmul -- hipBLASLt --
+    on the same bf16 operands beside it as context), with fractions of the
+    dense bf16 MFMA peak."""
+    from paper_2607_28144_amd import dit, synth
+    P = DIT
+    S, C, F = P["S"], P["C"], P["F"]
+    stream = torch.cuda.current_stream(dev)
+
+    def to_dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    params = {n: to_dev(v) for n, v in synth.dit_params(P["seed_params"]).items()}
+    x, e, kc, vc = synth.dit_inputs(P["seed_inputs"], S, P["ctx"], steps=P["steps"])
+    x0 = torch.from_numpy(x).to(dev)
+    xs = x0.clone()
+    es = [torch.from_numpy(e[i]).to(dev) for i in range(P["steps"])]
+    dk, dv = to_dev(kc), to_dev(vc)
+    blk = dit.DitBlock(params, heads=P["heads"])
+
+    def four_steps():
+        for i in range(P["steps"]):
+            blk.forward(xs, es[i], dk, dv, P["grid"])
+
+    t = time_calls(torch, stream, four_steps, reps, warmup)
+    gemm_flops = 2.0 * S * (C * 3 * C + 3 * C * C + 2 * C * F)
+    attn = attn_flops(1, P["heads"], S, S, C // P["heads"]) + attn_flops(1, P["heads"], S, P["ctx"], C // P["heads"])
+    flops = P["steps"] * (gemm_flops + attn)
+    leg = dict(t, steps=P["steps"], gflop=flops / 1e9, tflops=flops / (t["ms_avg"] * 1e-3) / 1e12,
+               ms_per_step=t["ms_avg"] / P["steps"],
+               workload=f"DiT block forward x {P['steps']} steps: S={S} (7x30x52) C={C} (12 heads x 128) "
+                        f"FFN {F}, 512 context tokens, bf16 weights N(0, 0.02), fp32 residual stream")
+    leg["frac"] = leg["tflops"] / PEAK_BF16_TFLOPS
+    layers = {}
+    h = torch.randn(S, max(C, F), device=dev).to(torch.bfloat16)
+    for name, N, K, epi in [("qkv", 3 * C, C, "bias"), ("o", C, C, "gated_residual"), ("ffn_up", F, C, "bias_gelu"),
+                            ("ffn_down", C, F, "gated_residual")]:
+        a = h[:, :K].contiguous()
+        w = params["w_qkv" if name == "qkv" else {"o": "w_o", "ffn_up": "w_1", "ffn_down": "w_2"}[name]]
+        bias = params["b_qkv" if name == "qkv" else {"o": "b_o", "ffn_up": "b_1", "ffn_down": "b_2"}[name]]
+        out = torch.zeros(S, N, device=dev, dtype=torch.float32 if epi == "gated_residual" else torch.bfloat16)
+        gate = torch.ones(N, device=dev) if epi == "gated_residual" else None
+        tl = time_calls(torch, stream, lambda: dit.linear_fwd(a, w, bias, epi, gate=gate, out=out), reps, warmup)
+        tb = time_calls(torch, stream, lambda: torch.matmul(a, w.t()), reps, warmup)
+        g = 2.0 * S * N * K
+        layers[name] = {"M": S, "N": N, "K": K, "epilogue": epi, "ms_avg": tl["ms_avg"],
+                        "tflops": g / (tl["ms_avg"] * 1e-3) / 1e12,
+                        "frac": g / (tl["ms_avg"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                        "hipblaslt_matmul_ms": tb["ms_avg"]}
+    leg["linear_layers"] = layers
+    return leg
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=20, help="untimed steps (the clock settles under load)")
-    ap.add_argument("--only", choices=["self", "cross", "share", "ring", "dual", "cross2", "copy", "normrope"],
+    ap.add_argument("--only", choices=["self", "cross", "share", "ring", "dual", "cross2", "copy", "normrope",
+                                       "block"],
                     default=None,
                     help="time one component alone (for profiling); 'copy' runs a plain 1 GiB elementwise "
                          "copy kernel, the reference for scaling HBM byte counters; 'normrope' times the q/k "
@@ -336,6 +396,9 @@ def main():
         return
     if args.only == "normrope":
         normrope_bench(torch, dev, args)
+        return
+    if args.only == "block":
+        print(json.dumps({"dit_block_c5": dit_block_leg(torch, dev, args.steps, args.warmup)}), flush=True)
         return
 
     def to_dev(bits):
@@ -481,6 +544,7 @@ def main():
                                            o_parts, l_parts, o_share, o_cross, l_cross)
         del q, k, v, kc, vc, rq, rk, rv, o_parts, l_parts
         line["legs"] = config_legs(torch, api, synth, dev, to_dev, 30, 10)
+        line["legs"]["dit_block_c5"] = dit_block_leg(torch, dev, 10, 3)
     if not args.no_cpu_baseline and args.only is None:
         print("[bench] timing the oracle on the host cores", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
