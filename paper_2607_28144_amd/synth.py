@@ -104,3 +104,16 @@ def dit_inputs(seed: int, S: int, S_ctx: int, steps: int = 4):
     kc = normal_bf16(rng, (S_ctx, DIT_HEADS, DIT_WIDTH // DIT_HEADS))
     vc = normal_bf16(rng, (S_ctx, DIT_HEADS, DIT_WIDTH // DIT_HEADS))
     return x, e, kc, vc
+
+
+def vae_inputs(seed: int, T: int, H: int, W: int, C: int, layers: int = 2):
+    """A VAE decoder stage at latent resolution: activations bf16 bits
+    [T, H, W, C] ~ N(0, 1) (channels-last), and `layers` causal 3D
+    convolutions C -> C as bf16 bits, weights [C, 3, 3, 3, C] ~ N(0, 1 / (27 C))
+    (unit gain at initialization) and biases [C] ~ N(0, 0.02^2) (trained VAE
+    weights are not available)."""
+    rng = np.random.default_rng(seed)
+    x = normal_bf16(rng, (T, H, W, C))
+    convs = [(normal_bf16(rng, (C, 3, 3, 3, C), float(1.0 / np.sqrt(27 * C))), normal_bf16(rng, (C,), 0.02))
+             for _ in range(layers)]
+    return x, convs
