@@ -359,13 +359,65 @@ def dit_block_leg(torch, dev, reps, warmup):
     return leg
 
 
+VAE = dict(T=7, H=60, W=104, C=384, ty=2, tx=4, halo=4, band=2, layers=2, seed=33, share_tile=1)
+
+
+def vae_leg(torch, dev, reps, warmup):
+    """A VAE decoder stage at the window's latent resolution (7 frames of
+    60 x 104, 384 channels; two causal 3 x 3 x 3 convolutions with SiLU
+    between) split 2 x 4 with halo 4 and blend band 2: one tile's stack (one
+    GPU's share of the 8-way split), and all eight tiles (one batched launch
+    per layer) plus the blended gather (the whole stage on one GPU).  FLOPs
+    count every computed pixel of the tiles' regions (halo included):
+    2 x 27 x Cin x Cout per pixel and layer."""
+    from paper_2607_28144_amd import synth, vae
+    P = VAE
+    T, H, W, C = P["T"], P["H"], P["W"], P["C"]
+    stream = torch.cuda.current_stream(dev)
+
+    def to_dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    x, convs = synth.vae_inputs(P["seed"], T, H, W, C, P["layers"])
+    dx = to_dev(x)
+    layers = [(to_dev(w), to_dev(b)) for w, b in convs]
+    tiles, Hr, Wr = vae.split(H, W, P["ty"], P["tx"], P["halo"])
+    tl = list(tiles)
+    share = [tl[P["share_tile"]]]
+
+    def pixels(ts):
+        return sum(T * (t.reg_y1 - t.reg_y0) * (t.reg_x1 - t.reg_x0) for t in ts)
+
+    per_pix = 2.0 * 27 * C * C * P["layers"]
+    t1 = time_calls(torch, stream, lambda: vae.tile_stack(dx, layers, share, Hr, Wr), reps, warmup)
+    g1 = per_pix * pixels(share)
+    t8 = time_calls(torch, stream, lambda: vae.blend(vae.tile_stack(dx, layers, tl, Hr, Wr), tl, H, W, P["band"]),
+                    reps, warmup)
+    g8 = per_pix * pixels(tl)
+    y = vae.tile_stack(dx, layers, tl, Hr, Wr)
+    tb = time_calls(torch, stream, lambda: vae.blend(y, tl, H, W, P["band"]), reps, warmup)
+    blend_bytes = 2.0 * C * (pixels(tl) + T * H * W)   # upper bound: every region pixel read once, the plane written
+    leg = {
+        "workload": f"VAE stage at latent resolution T={T} H={H} W={W} C={C}, {P['layers']} causal 3x3x3 convs, "
+                    f"split {P['ty']}x{P['tx']} halo {P['halo']} band {P['band']}",
+        "one_tile": dict(t1, gflop=g1 / 1e9, tflops=g1 / (t1["ms_avg"] * 1e-3) / 1e12,
+                         frac=g1 / (t1["ms_avg"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                         pixels=pixels(share), note="one GPU's share of the 8-way split"),
+        "all_tiles_and_blend": dict(t8, gflop=g8 / 1e9, tflops=g8 / (t8["ms_avg"] * 1e-3) / 1e12,
+                                    frac=g8 / (t8["ms_avg"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS),
+        "blend": dict(tb, gbs=blend_bytes / (tb["ms_avg"] * 1e-3) / 1e9,
+                      frac=blend_bytes / (tb["ms_avg"] * 1e-3) / 1e9 / PEAK_HBM_GBS),
+    }
+    return leg
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=20, help="untimed steps (the clock settles under load)")
     ap.add_argument("--only", choices=["self", "cross", "share", "ring", "dual", "cross2", "copy", "normrope",
-                                       "block"],
+                                       "block", "vae"],
                     default=None,
                     help="time one component alone (for profiling); 'copy' runs a plain 1 GiB elementwise "
                          "copy kernel, the reference for scaling HBM byte counters; 'normrope' times the q/k "
@@ -399,6 +451,9 @@ def main():
         return
     if args.only == "block":
         print(json.dumps({"dit_block_c5": dit_block_leg(torch, dev, args.steps, args.warmup)}), flush=True)
+        return
+    if args.only == "vae":
+        print(json.dumps({"split_vae_tile": vae_leg(torch, dev, args.steps, args.warmup)}), flush=True)
         return
 
     def to_dev(bits):
@@ -545,6 +600,7 @@ def main():
         del q, k, v, kc, vc, rq, rk, rv, o_parts, l_parts
         line["legs"] = config_legs(torch, api, synth, dev, to_dev, 30, 10)
         line["legs"]["dit_block_c5"] = dit_block_leg(torch, dev, 10, 3)
+        line["legs"]["split_vae_tile"] = vae_leg(torch, dev, 20, 5)
     if not args.no_cpu_baseline and args.only is None:
         print("[bench] timing the oracle on the host cores", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(args.cpu_seconds)

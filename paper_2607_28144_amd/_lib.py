@@ -24,6 +24,12 @@ class AttnPlan(ctypes.Structure):
                 ("key_ranges", ctypes.c_int32), ("workspace_bytes", ctypes.c_int64)]
 
 
+class VaeTile(ctypes.Structure):
+    """regenvc_vae_tile: a tile's core and region (half-open row/column ranges)."""
+    _fields_ = [(n, ctypes.c_int32) for n in ("core_y0", "core_y1", "core_x0", "core_x1",
+                                              "reg_y0", "reg_y1", "reg_x0", "reg_x1")]
+
+
 DIT_PARAM_NAMES = ("w_mod", "b_mod", "w_qkv", "b_qkv", "w_qn", "w_kn", "w_o", "b_o", "w_n3", "b_n3", "w_qc",
                    "b_qc", "w_qcn", "w_oc", "b_oc", "w_1", "b_1", "w_2", "b_2")
 
@@ -69,6 +75,12 @@ _SIGNATURES = {
                              _i32, _i32, ctypes.c_float, ctypes.c_void_p],
     "regenvc_dit_modulation": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, _i32, _i32,
                                ctypes.c_void_p],
+    "regenvc_vae_split": [_i32, _i32, _i32, _i32, _i32, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32),
+                          ctypes.POINTER(ctypes.c_int32)],
+    "regenvc_vae_conv3d_fwd": [ctypes.c_void_p, _i32, ctypes.c_void_p, ctypes.c_void_p, _i32, ctypes.c_void_p,
+                               _i32, _i32, _i32, _i32, _i32, ctypes.c_void_p, _i32, _i32, _i32, ctypes.c_void_p],
+    "regenvc_vae_blend": [ctypes.c_void_p, ctypes.c_void_p, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32,
+                          ctypes.c_void_p, ctypes.c_void_p],
     "regenvc_dit_block_workspace": [_i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_int64)],
     "regenvc_dit_block_fwd": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                               _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, ctypes.c_void_p,

@@ -12,7 +12,8 @@ REPO_DIR = os.path.dirname(PKG_DIR)
 CSRC = os.path.join(PKG_DIR, "csrc")
 LIB_NAME = "libregenvc_attn.so"
 LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
-SOURCES = ["api.cpp", "attn_fwd.hip", "lse_merge.hip", "norm_rope.hip", "dit_api.cpp", "dit.hip"]
+SOURCES = ["api.cpp", "attn_fwd.hip", "lse_merge.hip", "norm_rope.hip", "dit_api.cpp", "dit.hip", "vae_api.cpp",
+           "vae.hip"]
 ARCH = "gfx950"
 
 

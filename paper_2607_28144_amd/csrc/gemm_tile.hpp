@@ -1,0 +1,237 @@
+// The bf16 MFMA tile kernel shared by the linear layers of the diffusion
+// block (dense rows) and the VAE's causal 3D convolution (rows gathered as
+// an implicit GEMM): out[m][n] = epilogue(sum_k A[m][k] W[n][k]).
+//
+// Workgroup = 8 waves (two per SIMD) = one BM x BN output tile, BN = 64 WN;
+// the waves form an (8 / WN) x WN grid, each owning (BM / (8 / WN)) rows x
+// 64 channels on v_mfma_f32_16x16x32_bf16.  The product is formed
+// transposed, C^T = W A^T, so that a lane's accumulator holds four
+// consecutive output channels of one row (what the epilogues want).  K
+// advances in steps of 64: both operand tiles go HBM -> LDS with
+// global_load_lds_dwordx4 (no register staging) into a double-buffered LDS
+// ring; rows are 128 bytes, 16-byte chunk c of row r stored at chunk
+// c ^ ((r >> 1) & 7), which makes the fragment reads (16 rows, one chunk)
+// bank-conflict free.  Tiles are dealt XCD-aware: each XCD takes a
+// contiguous range of tiles (row blocks across all channel blocks), so the
+// rows it reads stay in its L2.
+//
+// The A source is a policy: for each of this lane's copy rows it gives the
+// address of the 16 bytes to copy at K step kt (a dense row, or a tap of a
+// convolution patch, or a page of zeros for padding).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace regenvc {
+namespace tile {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+typedef __attribute__((address_space(3))) char lds_char;
+
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kBK = 64;               // K per step (two 32-deep MFMA steps)
+constexpr int kRowBytes = kBK * 2;
+
+enum Epi : int32_t {
+    kBias = 0,        // out bf16 = y + bias
+    kBiasGelu = 1,    // out bf16 = gelu_tanh(y + bias)
+    kGatedRes = 2,    // out f32 (in place) = out + gate[n] * (y + bias[n])   (gate may be null: 1)
+    kBiasSilu = 3,    // out bf16 = silu(y + bias)
+};
+
+// Output side of a tile launch.
+struct Out {
+    const uint16_t *w;    // [N, K] bf16, K contiguous
+    const uint16_t *bias; // [N] bf16 or null
+    const float *gate;    // [N] f32 or null (kGatedRes)
+    void *out;            // bf16 or f32 [M, N], row stride ldo
+    int64_t ldo;
+    int32_t M, N, K;
+};
+
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// 16-byte HBM -> LDS copy (global_load_lds_dwordx4): lane i's 16 bytes land
+// at lds_base + 16 * i.  Inline asm so that the compiler does not order it
+// against the LDS reads of the other ring stage; completion is awaited with
+// an explicit s_waitcnt vmcnt before the barrier that publishes the stage.
+__device__ __forceinline__ void lds_copy16(const void *gptr, uint32_t lds_base)
+{
+    const uint32_t base = __builtin_amdgcn_readfirstlane(lds_base);  // wave-uniform by construction
+    __asm__ volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" : : "s"(base), "v"(gptr) : "m0");
+}
+#pragma clang diagnostic pop
+
+__device__ __forceinline__ void wait_all_copies()
+{
+    __asm__ volatile("s_waitcnt vmcnt(0)" : : : "memory");
+}
+
+__device__ __forceinline__ int swz(int row, int chunk)
+{
+    return chunk ^ ((row >> 1) & 7);
+}
+
+__device__ __forceinline__ float gelu_tanh(float x)
+{
+    // x/2 (1 + tanh(u)), tanh(u) = 1 - 2 / (e^(2u) + 1); u = sqrt(2/pi) (x + 0.044715 x^3)
+    const float u = 0.7978845608028654f * fmaf(0.044715f * x, x * x, x);
+    const float t = 1.0f - 2.0f / (__expf(2.0f * u) + 1.0f);
+    return 0.5f * x * (1.0f + t);
+}
+
+__device__ __forceinline__ float silu(float x)
+{
+    return x / (1.0f + __expf(-x));
+}
+
+__device__ __forceinline__ float bf(uint16_t b)
+{
+    return __uint_as_float(((uint32_t)b) << 16);
+}
+
+template <int BM, int WN, int EPI, class ASrc>
+__device__ __forceinline__ void tile_body(const ASrc &asrc, const Out &o, int tiles_n, int n_tiles, char *smem)
+{
+    constexpr int BN = 64 * WN;
+    constexpr int WGM = kWaves / WN;     // waves along M
+    constexpr int WM = BM / WGM;         // rows per wave
+    constexpr int MB = WM / 16;          // 16-row MFMA blocks per wave
+    constexpr int NB = 4;                // 16-channel MFMA blocks per wave
+    constexpr int A_BYTES = BM * kRowBytes;
+    constexpr int W_BYTES = BN * kRowBytes;
+    constexpr int STAGE = A_BYTES + W_BYTES;
+    constexpr int A_INSTR = A_BYTES / 1024;  // 1 KB (8 rows) per wave copy instruction
+    constexpr int W_INSTR = W_BYTES / 1024;
+    constexpr int A_PER = (A_INSTR + kWaves - 1) / kWaves;
+    constexpr int W_PER = W_INSTR / kWaves;
+    static_assert(WM % 16 == 0 && W_INSTR % kWaves == 0, "tile shape");
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = wave / WN, wn = wave % WN;
+    const int g = lane >> 4, x = lane & 15;
+
+    // XCD-aware tile: workgroup i runs on XCD i % 8; XCD x takes a contiguous
+    // range of tiles, channel blocks fastest
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int tile = xcd * (n_tiles >> 3) + min(xcd, n_tiles & 7) + slot;
+    const int tm = tile / tiles_n, tn = tile % tiles_n;
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    // this lane's copies: instruction j of a tile covers its rows 8j..8j+7;
+    // lane l fills LDS chunk l % 8 of row 8j + l / 8, which holds global
+    // chunk swz(row, l % 8).  Rows past the end re-read the last row (never
+    // stored).
+    typename ASrc::Row arow[A_PER];
+#pragma unroll
+    for (int i = 0; i < A_PER; ++i) {
+        const int j = min(wave + i * kWaves, A_INSTR - 1);
+        const int r = j * 8 + (lane >> 3);
+        arow[i] = asrc.row(min(m0 + r, o.M - 1), swz(r, lane & 7));
+    }
+    const uint16_t *wsrc[W_PER];
+#pragma unroll
+    for (int i = 0; i < W_PER; ++i) {
+        const int r = (wave + i * kWaves) * 8 + (lane >> 3);
+        const int gr = min(n0 + r, o.N - 1);
+        wsrc[i] = o.w + (int64_t)gr * o.K + swz(r, lane & 7) * 8;
+    }
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char *)smem;
+    auto issue = [&](int kt, int st) {
+        const uint32_t sa = lds0 + st * STAGE, sw = sa + A_BYTES;
+#pragma unroll
+        for (int i = 0; i < A_PER; ++i) {
+            const int j = wave + i * kWaves;
+            if (j < A_INSTR) lds_copy16(asrc.src(arow[i], kt), sa + j * 1024);
+        }
+#pragma unroll
+        for (int i = 0; i < W_PER; ++i) lds_copy16(wsrc[i] + kt * kBK, sw + (wave + i * kWaves) * 1024);
+    };
+
+    f32x4 acc[NB][MB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int nk = o.K / kBK;
+    issue(0, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+        const int st = kt & 1;
+        wait_all_copies();   // this wave's copies of step kt landed
+        __syncthreads();     // ... and every wave's; step kt-1's stage is free
+        if (kt + 1 < nk) issue(kt + 1, st ^ 1);
+        const lds_char *sa = (const lds_char *)smem + st * STAGE;
+        const lds_char *sw = sa + A_BYTES;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const int ch = ks * 4 + g;
+            bf16x8 wf[NB];
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+                const int r = wn * 64 + nb * 16 + x;
+                wf[nb] = *(const lds_bf16x8 *)(sw + r * kRowBytes + swz(r, ch) * 16);
+            }
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+                const int r = wm * WM + mb * 16 + x;
+                const bf16x8 af = *(const lds_bf16x8 *)(sa + r * kRowBytes + swz(r, ch) * 16);
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+                    acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[nb], af, acc[nb][mb], 0, 0, 0);
+            }
+        }
+    }
+
+    // epilogue: acc[nb][mb][i] = y[m0 + wm*WM + mb*16 + x][n0 + wn*64 + nb*16 + 4g + i]
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+        const int n = n0 + wn * 64 + nb * 16 + 4 * g;
+        if (n >= o.N) continue;
+        f32x4 bv = {0.f, 0.f, 0.f, 0.f};
+        if (o.bias != nullptr) {
+            const uint64_t b4 = *reinterpret_cast<const uint64_t *>(o.bias + n);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) bv[i] = bf((uint16_t)(b4 >> (16 * i)));
+        }
+        f32x4 gv = {1.f, 1.f, 1.f, 1.f};
+        if (EPI == kGatedRes && o.gate != nullptr) gv = *reinterpret_cast<const f32x4 *>(o.gate + n);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            const int m = m0 + wm * WM + mb * 16 + x;
+            if (m >= o.M) continue;
+            const f32x4 y = acc[nb][mb] + bv;
+            if constexpr (EPI == kGatedRes) {
+                f32x4 *p = reinterpret_cast<f32x4 *>(static_cast<float *>(o.out) + (int64_t)m * o.ldo + n);
+                *p = *p + gv * y;
+            } else {
+                bf16x4 w;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    w[i] = (__bf16)(EPI == kBiasGelu ? gelu_tanh(y[i]) : EPI == kBiasSilu ? silu(y[i]) : y[i]);
+                *reinterpret_cast<bf16x4 *>(static_cast<uint16_t *>(o.out) + (int64_t)m * o.ldo + n) = w;
+            }
+        }
+    }
+}
+
+// LDS bytes of a BM x BN tile's double-buffered ring.
+template <int BM, int WN>
+constexpr int lds_bytes()
+{
+    return 2 * (BM + 64 * WN) * kRowBytes;
+}
+
+// XCD-aware tile count helpers for the launchers.
+inline int tiles_along(int n, int b)
+{
+    return (n + b - 1) / b;
+}
+
+}  // namespace tile
+}  // namespace regenvc

@@ -21,7 +21,8 @@ def lib():
 
 
 def declared_functions():
-    text = open(HEADER).read() + open(os.path.join(REPO, "include", "regenvc_dit.h")).read()
+    text = "".join(open(os.path.join(REPO, "include", h)).read()
+                   for h in ("regenvc_attn.h", "regenvc_dit.h", "regenvc_vae.h"))
     return sorted(set(re.findall(r"^\s*(?:regenvc_status|const char \*|int64_t)\s*(regenvc_\w+)\s*\(", text, re.M)))
 
 
