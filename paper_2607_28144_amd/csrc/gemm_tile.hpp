@@ -12,8 +12,9 @@
 // ring; rows are 128 bytes, 16-byte chunk c of row r stored at chunk
 // c ^ ((r >> 1) & 7), which makes the fragment reads (16 rows, one chunk)
 // bank-conflict free.  Tiles are dealt XCD-aware: each XCD takes a
-// contiguous range of tiles (row blocks across all channel blocks), so the
-// rows it reads stay in its L2.
+// contiguous range of tiles, numbered in groups of four row blocks swept
+// across the channel blocks, so that the tiles resident on an XCD share
+// their operand blocks through its L2.
 //
 // The A source is a policy: for each of this lane's copy rows it gives the
 // address of the 16 bytes to copy at K step kt (a dense row, or a tap of a
@@ -35,6 +36,7 @@ constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kBK = 64;               // K per step (two 32-deep MFMA steps)
 constexpr int kRowBytes = kBK * 2;
+constexpr int kGroupM = 4;            // row blocks per group of the tile order
 
 enum Epi : int32_t {
     kBias = 0,        // out bf16 = y + bias
@@ -117,10 +119,17 @@ __device__ __forceinline__ void tile_body(const ASrc &asrc, const Out &o, int ti
     const int g = lane >> 4, x = lane & 15;
 
     // XCD-aware tile: workgroup i runs on XCD i % 8; XCD x takes a contiguous
-    // range of tiles, channel blocks fastest
+    // range of tiles.  Tiles are numbered in groups of kGroupM row blocks
+    // swept across the channel blocks (row block fastest), so the ~32 tiles
+    // resident on an XCD at a time cover about 4 row blocks x 8 channel
+    // blocks: each A row block and W block they read serves several of them
+    // from the XCD's L2.
     const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
     const int tile = xcd * (n_tiles >> 3) + min(xcd, n_tiles & 7) + slot;
-    const int tm = tile / tiles_n, tn = tile % tiles_n;
+    const int tiles_m = n_tiles / tiles_n;
+    const int group = tile / (kGroupM * tiles_n), in_group = tile - group * kGroupM * tiles_n;
+    const int gm = min(tiles_m - group * kGroupM, kGroupM);
+    const int tm = group * kGroupM + in_group % gm, tn = in_group / gm;
     const int m0 = tm * BM, n0 = tn * BN;
 
     // this lane's copies: instruction j of a tile covers its rows 8j..8j+7;
@@ -168,23 +177,36 @@ __device__ __forceinline__ void tile_body(const ASrc &asrc, const Out &o, int ti
         if (kt + 1 < nk) issue(kt + 1, st ^ 1);
         const lds_char *sa = (const lds_char *)smem + st * STAGE;
         const lds_char *sw = sa + A_BYTES;
+        // the step's 2 x MB groups of 4 MFMAs (k half ks, row block mb),
+        // each A fragment read two groups ahead of its MFMAs (a ring of 3)
+        // and the second k half's W fragments read at the start, the order
+        // pinned so that the LDS latency passes under earlier MFMAs
+        auto afrag = [&](int s) {
+            const int r = wm * WM + (s % MB) * 16 + x;
+            return *(const lds_bf16x8 *)(sa + r * kRowBytes + swz(r, (s / MB) * 4 + g) * 16);
+        };
+        auto wfrag = [&](int ks, int nb) {
+            const int r = wn * 64 + nb * 16 + x;
+            return *(const lds_bf16x8 *)(sw + r * kRowBytes + swz(r, ks * 4 + g) * 16);
+        };
+        bf16x8 wf[2][NB], ar[3];
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            const int ch = ks * 4 + g;
-            bf16x8 wf[NB];
+        for (int nb = 0; nb < NB; ++nb) wf[0][nb] = wfrag(0, nb);
+        ar[0] = afrag(0);
+        ar[1] = afrag(1);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-                const int r = wn * 64 + nb * 16 + x;
-                wf[nb] = *(const lds_bf16x8 *)(sw + r * kRowBytes + swz(r, ch) * 16);
+        for (int s = 0; s < 2 * MB; ++s) {
+            if (s + 2 < 2 * MB) ar[(s + 2) % 3] = afrag(s + 2);
+            if (s == 0) {
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) wf[1][nb] = wfrag(1, nb);
             }
+            const int ks = s / MB, mb = s % MB;
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb) {
-                const int r = wm * WM + mb * 16 + x;
-                const bf16x8 af = *(const lds_bf16x8 *)(sa + r * kRowBytes + swz(r, ch) * 16);
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb)
-                    acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[nb], af, acc[nb][mb], 0, 0, 0);
-            }
+            for (int nb = 0; nb < NB; ++nb)
+                acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[ks][nb], ar[s % 3], acc[nb][mb], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
 
