@@ -1331,6 +1331,13 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
         __asm__ volatile("" : "+v"(p[0][0]), "+v"(p[0][1]), "+v"(p[1][0]), "+v"(p[1][1]));
         __builtin_amdgcn_sched_barrier(0);
     };
+    // The barriers after a wave's last M phase: no score or weight register
+    // is live any more, so nothing is pinned.
+    auto end_barrier = [&]() __attribute__((always_inline)) {
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+        __builtin_amdgcn_sched_barrier(0);
+    };
 
     // Prologue: tiles 0 and 1 in flight, tile 0 landed.
     issue_next();
@@ -1347,6 +1354,10 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     // it: V fragments of its tile u-1, which landed a pair earlier and is not
     // overwritten before pair u+1.  The M phase runs at raised priority.
     if (grp == 0) {
+        // (distinct markers at the head of the two schedules: their common
+        // first reads are not hoisted above the branch, which would keep
+        // them live through the other group's whole schedule)
+        __asm__ volatile("; group 0 schedule");
         mprefetch(st(0), st(0), F_{});
         __builtin_amdgcn_s_setprio(1);
         mphase(st(0), st(0), F_{}, T_{});
@@ -1383,11 +1394,13 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
             phase_barrier();
         }
         __builtin_amdgcn_s_setprio(1);
+        __asm__ volatile("; last M phase, group 0");  // keeps the two groups' last M phases apart
         mphase(st(T), st(T - 1), T_{}, F_{});
         __builtin_amdgcn_s_setprio(0);
-        phase_barrier();
-        phase_barrier();
+        end_barrier();
+        end_barrier();
     } else {
+        __asm__ volatile("; group 1 schedule");
         mprefetch(st(0), st(0), F_{});
         phase_barrier();
         __builtin_amdgcn_s_setprio(1);
@@ -1411,13 +1424,22 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
         mprefetch(st(T), st(T - 1), T_{});
         phase_barrier();
         __builtin_amdgcn_s_setprio(1);
+        __asm__ volatile("; last M phase, group 1");
         mphase(st(T), st(T - 1), T_{}, F_{});
         __builtin_amdgcn_s_setprio(0);
         issue_next();
         wait_vmcnt<PER_TILE>();
-        phase_barrier();
+        end_barrier();
     }
     wait_vmcnt<0>();  // the clamped trailing copies must land before the workgroup exits
+
+    // The epilogue's lane indices come from a fresh copy of the thread index
+    // (opaque to the compiler), so that no index or address computed before
+    // the key loop has to stay live across it.
+    int tid_e = (int)threadIdx.x;
+    __asm__ volatile("" : "+v"(tid_e));
+    const int lane_e = tid_e & 63, x_e = lane_e & 15, g_e = lane_e >> 4;
+    const int qrow0_e = wave * 32 + x_e, qi0_e = qt * BM + qrow0_e;
 
     // Epilogue: per query, l and l_r = the sums of the four lanes' partial
     // sums; O = O^T / l_r, LSE = ln2 * (m_ref + log2 l); a split tile's key
@@ -1430,7 +1452,7 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
                 const float lt = quad_sum(lsum[qb]);
                 float sc = 1.0f / quad_sum(rsum[qb]);
                 float lse_val = (mref[qb] + __log2f(lt)) * kLn2;
-                const int qi = qi0 + qb * 16;
+                const int qi = qi0_e + qb * 16;
                 if constexpr (ACC) {
                     const int qc = min(qi, a.Sq - 1);
                     const RunMerge m = run_merge(a.run_lse[((int64_t)b * a.H + h) * a.Sq + qc], lse_val);
@@ -1438,7 +1460,7 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
                     sc *= m.wc;
                     wr[qb] = m.run ? m.wr : -1.f;
                 }
-                if (a.lse != nullptr && g == 0 && qi < a.Sq) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = lse_val;
+                if (a.lse != nullptr && g_e == 0 && qi < a.Sq) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = lse_val;
 #pragma unroll
                 for (int db = 0; db < DB; ++db) oacc[db][qb] *= sc;
             }
@@ -1450,20 +1472,20 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
 #pragma unroll
                 for (int db = 0; db < DB; ++db) {
                     if constexpr (OUT_F32) {
-                        stage_out4_f32<D>(stg, qb * 16 + x, db * 16 + g * 4, oacc[db][qb]);
+                        stage_out4_f32<D>(stg, qb * 16 + x_e, db * 16 + g_e * 4, oacc[db][qb]);
                     } else {
                         bf16x4 w;
 #pragma unroll
                         for (int e = 0; e < 4; ++e) w[e] = (__bf16)oacc[db][qb][e];
-                        stage_out4<D>(stg, qb * 16 + x, db * 16 + g * 4, w);
+                        stage_out4<D>(stg, qb * 16 + x_e, db * 16 + g_e * 4, w);
                     }
                 }
             if constexpr (ACC)
-                store_staged_rows_run<D, OUT_F32>(a, stg, lane, b, h, qt * BM + wave * 32, wr);
+                store_staged_rows_run<D, OUT_F32>(a, stg, lane_e, b, h, qt * BM + wave * 32, wr);
             else if constexpr (OUT_F32)
-                store_staged_rows_f32<D>(a, stg, lane, b, h, qt * BM + wave * 32);
+                store_staged_rows_f32<D>(a, stg, lane_e, b, h, qt * BM + wave * 32);
             else
-                store_staged_rows<D>(a, stg, lane, b, h, qt * BM + wave * 32);
+                store_staged_rows<D>(a, stg, lane_e, b, h, qt * BM + wave * 32);
             return;
         }
     }
@@ -1472,12 +1494,12 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     for (int qb = 0; qb < 2; ++qb) {
         const float lt = quad_sum(lsum[qb]);
         const float inv = 1.0f / quad_sum(rsum[qb]);
-        const int qrow = qrow0 + qb * 16, qi = qi0 + qb * 16;
+        const int qrow = qrow0_e + qb * 16, qi = qi0_e + qb * 16;
         if (qi >= a.Sq) continue;
         float *orow = pl.ws_o + ((int64_t)slot * BM + qrow) * D;
 #pragma unroll
-        for (int db = 0; db < DB; ++db) *reinterpret_cast<f32x4 *>(orow + db * 16 + g * 4) = oacc[db][qb] * inv;
-        if (g == 0) pl.ws_lse[(int64_t)slot * BM + qrow] = (mref[qb] + __log2f(lt)) * kLn2;
+        for (int db = 0; db < DB; ++db) *reinterpret_cast<f32x4 *>(orow + db * 16 + g_e * 4) = oacc[db][qb] * inv;
+        if (g_e == 0) pl.ws_lse[(int64_t)slot * BM + qrow] = (mref[qb] + __log2f(lt)) * kLn2;
     }
 }
 

@@ -145,6 +145,46 @@ __global__ __launch_bounds__(256) void rms_norm_kernel(RmsNormArgs a)
 }
 
 // adaLN vectors: one wave per output row j, lanes over the C inputs.
+// Vector form (C a multiple of 8, 16-byte aligned rows and e): each wave
+// takes kModRows consecutive rows; a lane walks 8-channel chunks, forms
+// silu(e) of a chunk once and applies it to the chunk of every one of its
+// rows (16-byte weight loads, kModRows in flight).
+constexpr int kModRows = 4;
+
+__global__ __launch_bounds__(256) void modulation_vec_kernel(ModulationArgs a)
+{
+    const int lane = threadIdx.x & 63;
+    const int j0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kModRows;
+    if (j0 >= a.rows) return;
+    const int nr = min(kModRows, a.rows - j0);
+    const uint16_t *w = static_cast<const uint16_t *>(a.w) + (int64_t)j0 * a.C;
+    float s[kModRows] = {};
+    for (int c = lane * 8; c < a.C; c += 64 * 8) {
+        const f32x4 e0 = *reinterpret_cast<const f32x4 *>(a.e + c);
+        const f32x4 e1 = *reinterpret_cast<const f32x4 *>(a.e + c + 4);
+        float u[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            u[i] = e0[i] / (1.0f + __expf(-e0[i]));
+            u[4 + i] = e1[i] / (1.0f + __expf(-e1[i]));
+        }
+#pragma unroll
+        for (int r = 0; r < kModRows; ++r) {
+            if (r < nr) {
+                const bf16x8 v = *reinterpret_cast<const bf16x8 *>(w + (int64_t)r * a.C + c);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) s[r] = fmaf((float)v[i], u[i], s[r]);
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < kModRows; ++r) {
+        const float t = wave_sum(s[r]);
+        if (lane == 0 && r < nr) a.mod[j0 + r] = t + bf(static_cast<const uint16_t *>(a.b)[j0 + r]);
+    }
+}
+
+// Scalar form, any C and alignment: one wave per row.
 __global__ __launch_bounds__(256) void modulation_kernel(ModulationArgs a)
 {
     const int lane = threadIdx.x & 63;
@@ -240,7 +280,14 @@ hipError_t launch_rms_norm(const RmsNormArgs &a, hipStream_t stream)
 
 hipError_t launch_modulation(const ModulationArgs &a, hipStream_t stream)
 {
-    hipLaunchKernelGGL(modulation_kernel, dim3((unsigned)((a.rows + 3) / 4)), dim3(256), 0, stream, a);
+    const bool vec = a.C % 8 == 0 && ((uintptr_t)a.w & 15) == 0 && ((uintptr_t)a.e & 15) == 0;
+    if (vec) {
+        const int per_block = 4 * kModRows;
+        hipLaunchKernelGGL(modulation_vec_kernel, dim3((unsigned)((a.rows + per_block - 1) / per_block)), dim3(256), 0,
+                           stream, a);
+    } else {
+        hipLaunchKernelGGL(modulation_kernel, dim3((unsigned)((a.rows + 3) / 4)), dim3(256), 0, stream, a);
+    }
     return hipGetLastError();
 }
 

@@ -152,6 +152,22 @@ def test_modulation_vectors():
                 2 * ACC * (np.abs(odit.widen(w)) @ np.abs(s)) + 1e-7)
 
 
+def test_modulation_vectors_any_width():
+    """Widths that are not a multiple of 8 (and a row count that is not a
+    multiple of the rows per wave) take the scalar form of the kernel; the
+    vector form's partial last group of rows is covered by 6 x 1536 - 4 rows."""
+    rng = np.random.default_rng(9)
+    for rows, C in [(21, 100), (6 * 1536 - 4, 1536)]:
+        w, b = bits(rng, (rows, C), 0.02), bits(rng, (rows,), 0.02)
+        e = rng.standard_normal(C).astype(np.float32)
+        out = kern().modulation(dev_bits(w).view(rows, C), dev_bits(b), torch.from_numpy(e).cuda())
+        torch.cuda.synchronize()
+        s = odit.silu(e.astype(np.float64))
+        ref = odit.gemm(s[None, :], odit.widen(w), odit.widen(b)).reshape(-1)
+        check_bound(f"adaLN modulation rows={rows} C={C}", out.cpu().numpy().astype(np.float64), ref,
+                    2 * ACC * (np.abs(odit.widen(w)) @ np.abs(s)) + 1e-7)
+
+
 # ------------------------------------------------------------------ the block
 def device_block(params):
     return kern().DitBlock({n: dev_bits(v) for n, v in params.items()})
