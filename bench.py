@@ -166,9 +166,7 @@ def config_legs(torch, api, synth, dev, to_dev, steps, warmup):
     lse = torch.empty((P["B"], P["H"], P["Sq"]), dtype=torch.float32, device=dev)
 
     def paper_share():
-        for i in range(P["chunks"]):
-            a, b = bounds[i], bounds[i + 1]
-            api.attn_partial_fwd(q, k[:, a:b], v[:, a:b], scale=scale, out=o_parts[i], lse_out=l_parts[i])
+        api.attn_partials_fwd(q, k, v, bounds, scale=scale, outs=o_parts, lse_outs=l_parts)
         api.lse_merge(o_parts, l_parts, out=o, lse_out=lse)
 
     t = time_calls(torch, stream, paper_share, steps, warmup)
@@ -177,7 +175,7 @@ def config_legs(torch, api, synth, dev, to_dev, steps, warmup):
     legs["paper_share_h3_sq5460_chunks2x5460"] = dict(
         t, gflop=g / 1e9, tflops=tf, frac=tf / PEAK_BF16_TFLOPS,
         workload="rank share of the 12-head model under Ulysses 4 x Ring 2: H=3, Sq=5460, keys in 2 chunks "
-                 "of 5460, 2 partials (f32) + LSE merge (bf16)")
+                 "of 5460, both partials (f32) in one launch + LSE merge (bf16)")
     return legs
 
 
@@ -270,6 +268,10 @@ def next_steps_timing(torch, api, synth, dev, to_dev, q, kc, vc, rq, rk, rv, sca
             api.attn_partial_fwd(rq, rk[:, a:b], rv[:, a:b], scale=scale, out=o_parts[i], lse_out=l_parts[i])
         api.lse_merge(o_parts, l_parts, out=o_share)
 
+    def share_one_launch():
+        api.attn_partials_fwd(rq, rk, rv, bounds, scale=scale, outs=o_parts, lse_outs=l_parts)
+        api.lse_merge(o_parts, l_parts, out=o_share)
+
     def two_calls():
         api.cross_attn_fwd(q, kc, vc, scale=scale, out=o_cross, lse_out=l_cross)
         api.cross_attn_fwd(q, ki, vi, scale=scale, out=o_img, lse_out=l_img)
@@ -280,7 +282,8 @@ def next_steps_timing(torch, api, synth, dev, to_dev, q, kc, vc, rq, rk, rv, sca
     # each pair is timed alternately, in blocks, under the same conditions
     gs = attn_flops(1, SHARE["H"], SHARE["S"], SHARE["S"], SHARE["D"]) / 1e9
     gd = attn_flops(B, H, S, W["ctx"] + W["img"], D) / 1e9
-    cases = [("share_partials_merge", share, gs), ("share_ring", ring, gs),
+    cases = [("share_partials_merge", share, gs), ("share_partials_one_launch_merge", share_one_launch, gs),
+             ("share_ring", ring, gs),
              ("cross_two_calls_512_257", two_calls, gd), ("dual_cross_512_257", dual, gd)]
     ms = {name: [] for name, _, _ in cases}
     stream = torch.cuda.current_stream(dev)
@@ -508,10 +511,8 @@ def main():
             elif c == "cross2":
                 api.cross_attn_fwd(q, kc, vc, scale=scale, out=o_cross, lse_out=l_cross)
                 api.cross_attn_fwd(q, ki, vi, scale=scale, out=o_self, lse_out=l_img)
-            elif c == "share":
-                for i in range(nch):
-                    a, b = bounds[i], bounds[i + 1]
-                    api.attn_partial_fwd(rq, rk[:, a:b], rv[:, a:b], scale=scale, out=o_parts[i], lse_out=l_parts[i])
+            elif c == "share":  # every chunk's partial in one launch, then the merge
+                api.attn_partials_fwd(rq, rk, rv, bounds, scale=scale, outs=o_parts, lse_outs=l_parts)
                 api.lse_merge(o_parts, l_parts, out=o_share, lse_out=l_share)
             else:  # the same share with the merge fused into each chunk's epilogue
                 api.attn_partial_fwd(rq, rk[:, :bounds[1]], rv[:, :bounds[1]], scale=scale, out=o_parts[0],
@@ -582,7 +583,7 @@ def main():
         "config": {
             "workload": "window self-attention B=1 S=10920 (7x30x52) H=12 d=128 bf16 O + LSE (value); one step "
                         "also runs the cross-attention to 512 ctx tokens and one rank share (H=5, 4 key chunks "
-                        "of 2730, partials + LSE merge)"
+                        "of 2730, every partial in one launch + LSE merge)"
             if args.only is None else f"component '{args.only}' only",
             "value_is": f"components.{dom}: algorithmic FLOPs / average call duration (HIP events)",
             "components": comps, "B": B, "H": H, "S": S, "d": D, "ctx": W["ctx"],

@@ -8,7 +8,8 @@
  *   - Ring passes key/value blocks between GPUs and folds their results
  *     together with running-max rescaling: one partial result per key/value
  *     chunk, then a log-sum-exp merge, exact apart from summation order
- *                            -> regenvc_attn_partial_fwd + regenvc_lse_merge,
+ *                            -> regenvc_attn_partial_fwd (or every chunk's at
+                               once: regenvc_attn_partials_fwd) + regenvc_lse_merge,
  *                               or regenvc_attn_ring_accumulate (merge fused)
  *   - the conditioning path (Sec. 3.9, "Hybrid CPU-GPU deployment") streams
  *     precomputed text/image key/value tensors to the GPU, which the video
@@ -151,6 +152,33 @@ regenvc_status regenvc_attn_partial_fwd(const regenvc_tensor *q,
                                         int32_t B, int32_t H, int32_t Sq,
                                         int32_t Skv_chunk, int32_t D,
                                         float softmax_scale, void *stream);
+
+/* The partials of several key chunks in ONE launch (Sec. 3.5: a GPU that
+   holds all of its ring's key/value chunks -- e.g. after an all-gather --
+   can compute every chunk's partial at once).  Chunk c covers keys
+   [chunk_start[c], chunk_start[c+1]) of k and v (full [B,Skv,H,D] views);
+   its result is what regenvc_attn_partial_fwd gives on that chunk, up to
+   rounding (bitwise on the query tiles that both keep whole when every
+   chunk has the same number of 64-key tiles; tiles split along the keys to
+   fill the compute units are summed in another order).  One launch fills
+   the GPU where a chunk's query tiles alone would leave compute units
+   idle.
+     chunk_start: HOST array of num_chunks + 1 ascending key offsets,
+       0 <= chunk_start[0] and chunk_start[num_chunks] <= Skv; every chunk
+       holds at least one key (INVALID_ARG otherwise)
+     o_parts, lse_parts: HOST arrays of num_chunks DEVICE pointers;
+       o_parts[c]: f32 [B,Sq,H,D] contiguous, normalized over chunk c's keys;
+       lse_parts[c]: f32 [B,H,Sq] (the layout regenvc_lse_merge reads); no
+       part may overlap an input or another part
+     1 <= num_chunks <= REGENVC_MAX_PARTS
+   Scratch as the other attention calls (workspace_bytes of
+   regenvc_attn_partials_plan_query). */
+regenvc_status regenvc_attn_partials_fwd(const regenvc_tensor *q, const regenvc_tensor *k,
+                                         const regenvc_tensor *v, int32_t num_chunks,
+                                         const int32_t *chunk_start, float *const *o_parts,
+                                         float *const *lse_parts, int32_t B, int32_t H,
+                                         int32_t Sq, int32_t Skv, int32_t D, float softmax_scale,
+                                         void *stream);
 
 /* Log-sum-exp merge of num_parts partial results over disjoint key chunks
    into the result over their union (Sec. 3.5: the sharded computation equals
@@ -302,8 +330,18 @@ regenvc_status regenvc_cross_attn_dual_plan_query(int32_t B, int32_t H, int32_t 
                                                   int32_t S_img, int32_t D, int32_t n_cu,
                                                   regenvc_attn_plan *plan);
 
+/* Work plan of one regenvc_attn_partials_fwd call: query_tiles counts the
+   tiles of every chunk (num_chunks * B * H * ceil(Sq / 256)), key_tiles is
+   the last chunk's, and split tiles (the last ones of the launch) are split
+   only when every chunk they belong to has that many key tiles.  Host-only;
+   the chunk arguments as in regenvc_attn_partials_fwd. */
+regenvc_status regenvc_attn_partials_plan_query(int32_t B, int32_t H, int32_t Sq,
+                                                int32_t num_chunks, const int32_t *chunk_start,
+                                                int32_t D, int32_t n_cu, regenvc_attn_plan *plan);
+
 /* Binds a caller-owned DEVICE buffer of `bytes` bytes as the scratch memory
    of the attention calls (regenvc_attn_fwd, regenvc_attn_partial_fwd,
+   regenvc_attn_partials_fwd,
    regenvc_attn_ring_accumulate, regenvc_cross_attn_fwd,
    regenvc_cross_attn_dual_fwd) made later on the calling thread, until
    another binding replaces it; workspace == NULL unbinds (back to the pool).

@@ -55,6 +55,11 @@ _SIGNATURES = {
                                  _i32, _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_void_p],
     "regenvc_attn_partial_fwd": [_PT, _PT, _PT, _PT, ctypes.c_void_p,
                                  _i32, _i32, _i32, _i32, _i32, ctypes.c_float, ctypes.c_void_p],
+    "regenvc_attn_partials_fwd": [_PT, _PT, _PT, _i32, ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_void_p),
+                                  ctypes.POINTER(ctypes.c_void_p), _i32, _i32, _i32, _i32, _i32, ctypes.c_float,
+                                  ctypes.c_void_p],
+    "regenvc_attn_partials_plan_query": [_i32, _i32, _i32, _i32, ctypes.POINTER(_i32), _i32, _i32,
+                                         ctypes.POINTER(AttnPlan)],
     "regenvc_lse_merge": [ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(ctypes.c_void_p), _i32,
                           _PT, ctypes.c_int, ctypes.c_void_p, _i32, _i32, _i32, _i32, ctypes.c_void_p],
     "regenvc_attn_ring_accumulate": [_PT, _PT, _PT, _PT, ctypes.c_void_p, _PT, ctypes.c_int,

@@ -12,7 +12,7 @@ from __future__ import annotations
 
 import ctypes
 import math
-from typing import Optional, Sequence, Tuple
+from typing import List, Optional, Sequence, Tuple
 
 import torch
 
@@ -147,6 +147,65 @@ def attn_partial_fwd(q: torch.Tensor, k_chunk: torch.Tensor, v_chunk: torch.Tens
     """Partial attention over one key/value chunk (regenvc_attn_partial_fwd):
     float32 O normalized over the chunk, and its LSE."""
     return _attn("regenvc_attn_partial_fwd", q, k_chunk, v_chunk, scale, torch.float32, out, True, lse_out)
+
+
+def _chunk_plan(device: torch.device, B, H, Sq, bounds, D) -> int:
+    """Scratch bytes of one chunked-partials call (host-only plan query)."""
+    idx = device.index if device.index is not None else torch.cuda.current_device()
+    key = (idx, B, H, Sq, tuple(bounds), D)
+    need = _NEED.get(key)
+    if need is None:
+        if idx not in _N_CU:
+            _N_CU[idx] = torch.cuda.get_device_properties(idx).multi_processor_count
+        plan = _lib.AttnPlan()
+        arr = (ctypes.c_int32 * len(bounds))(*bounds)
+        st = _lib.load().regenvc_attn_partials_plan_query(B, H, Sq, len(bounds) - 1, arr, D, _N_CU[idx],
+                                                          ctypes.byref(plan))
+        need = _NEED[key] = plan.workspace_bytes if st == _lib.OK else 0
+    return need
+
+
+def attn_partials_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, bounds: Sequence[int],
+                      scale: Optional[float] = None, outs: Optional[Sequence[torch.Tensor]] = None,
+                      lse_outs: Optional[Sequence[torch.Tensor]] = None
+                      ) -> Tuple[List[torch.Tensor], List[torch.Tensor]]:
+    """Partials of every key chunk [bounds[c], bounds[c+1]) in one launch
+    (regenvc_attn_partials_fwd): per chunk, float32 O [B, Sq, H, D]
+    normalized over the chunk and its LSE [B, H, Sq], as
+    attn_partial_fwd gives chunk by chunk."""
+    B, Sq, H, D = q.shape
+    Skv = k.shape[1]
+    if tuple(k.shape) != (B, Skv, H, D) or tuple(v.shape) != (B, Skv, H, D):
+        raise ValueError(f"k/v shapes {tuple(k.shape)}, {tuple(v.shape)} do not match q {tuple(q.shape)}")
+    n = len(bounds) - 1
+    if n < 1:
+        raise ValueError("need at least one chunk (two bounds)")
+    if outs is None:
+        outs = [torch.empty((B, Sq, H, D), dtype=torch.float32, device=q.device) for _ in range(n)]
+    if lse_outs is None:
+        lse_outs = [torch.empty((B, H, Sq), dtype=torch.float32, device=q.device) for _ in range(n)]
+    if len(outs) != n or len(lse_outs) != n:
+        raise ValueError(f"{n} chunks need {n} outputs and {n} LSE outputs")
+    for t in outs:
+        if tuple(t.shape) != (B, Sq, H, D) or t.dtype != torch.float32 or not t.is_contiguous() \
+                or t.device != q.device:
+            raise ValueError("outs must be contiguous float32 [B, Sq, H, D] tensors on q's device")
+    for t in lse_outs:
+        if tuple(t.shape) != (B, H, Sq) or t.dtype != torch.float32 or not t.is_contiguous() \
+                or t.device != q.device:
+            raise ValueError("lse_outs must be contiguous float32 [B, H, Sq] tensors on q's device")
+    qd, kd, vd = _desc(q, "q", torch.bfloat16), _desc(k, "k", torch.bfloat16), _desc(v, "v", torch.bfloat16)
+    arr = (ctypes.c_int32 * (n + 1))(*[int(x) for x in bounds])
+    optrs = (ctypes.c_void_p * n)(*[t.data_ptr() for t in outs])
+    lptrs = (ctypes.c_void_p * n)(*[t.data_ptr() for t in lse_outs])
+    lib = _lib.load()
+    need = _chunk_plan(q.device, B, H, Sq, [int(x) for x in bounds], D)
+    with torch.cuda.device(q.device):
+        st = _with_workspace(q.device, need, lambda: lib.regenvc_attn_partials_fwd(
+            ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), n, arr, optrs, lptrs, B, H, Sq, Skv, D,
+            _scale(scale, D), _stream(q.device)))
+    _lib.check(st, "regenvc_attn_partials_fwd")
+    return list(outs), list(lse_outs)
 
 
 def attn_ring_accumulate(q: torch.Tensor, k_chunk: torch.Tensor, v_chunk: torch.Tensor, o_run: torch.Tensor,

@@ -166,6 +166,24 @@ struct Ctx2 {
     float *lse;  // may be null
 };
 
+// The bound workspace for a launch needing `need` bytes: too small, or
+// overlapping one of the call's n tensor extents, is INVALID_ARG.
+regenvc_status bound_workspace(const char *fn, size_t need, const Extent *ext, int n, regenvc::Workspace *ws)
+{
+    if ((size_t)g_ws_bytes < need)
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: the bound workspace holds %lld bytes, this call needs %zu", fn,
+                    (long long)g_ws_bytes, need);
+    if (need > 0) {
+        const Extent ew = flat_extent(g_ws_ptr, (int64_t)need, 1);
+        for (int i = 0; i < n; ++i)
+            if (overlap(ew, ext[i]))
+                return fail(REGENVC_ERR_INVALID_ARG, "%s: the bound workspace overlaps a tensor of the call", fn);
+    }
+    ws->ptr = g_ws_ptr;
+    ws->bytes = (size_t)g_ws_bytes;
+    return REGENVC_OK;
+}
+
 // run_o (ring accumulate only): f32 running output, read; lse is then the
 // running LSE, read and rewritten in place; o may be run_o itself (f32).
 // ctx2 (dual cross-attention only): the second context, summed into o.
@@ -313,21 +331,11 @@ regenvc_status attn_common(const char *fn, const regenvc_tensor *q, const regenv
         ws.ptr = p;
         ws.bytes = regenvc::kNoAllocScratchBytes;
     } else if (g_ws_ptr != nullptr) {
-        const size_t need = regenvc::attn_workspace_need(a);
-        if ((size_t)g_ws_bytes < need)
-            return fail(REGENVC_ERR_INVALID_ARG, "%s: the bound workspace holds %lld bytes, this call needs %zu", fn,
-                        (long long)g_ws_bytes, need);
-        if (need > 0) {
-            const Extent ew = flat_extent(g_ws_ptr, (int64_t)need, 1);
-            const bool hit = overlap(ew, eq) || overlap(ew, ek) || overlap(ew, ev) || overlap(ew, eo) ||
-                             overlap(ew, ek2) || overlap(ew, ev2) || overlap(ew, er) ||
-                             (lse != nullptr && overlap(ew, flat_extent(lse, (int64_t)B * H * Sq, 4))) ||
-                             (ctx2 != nullptr && ctx2->lse != nullptr &&
-                              overlap(ew, flat_extent(ctx2->lse, (int64_t)B * H * Sq, 4)));
-            if (hit) return fail(REGENVC_ERR_INVALID_ARG, "%s: the bound workspace overlaps a tensor of the call", fn);
-        }
-        ws.ptr = g_ws_ptr;
-        ws.bytes = (size_t)g_ws_bytes;
+        const int64_t nl = (int64_t)B * H * Sq;
+        const Extent none{0, 0};
+        const Extent ext[9] = {eq, ek, ev, eo, ek2, ev2, er, lse ? flat_extent(lse, nl, 4) : none,
+                               ctx2 && ctx2->lse ? flat_extent(ctx2->lse, nl, 4) : none};
+        if ((st = bound_workspace(fn, regenvc::attn_workspace_need(a), ext, 9, &ws)) != REGENVC_OK) return st;
     }
     return launched(regenvc::launch_attn(a, static_cast<hipStream_t>(stream), ws), fn);
 }
@@ -361,6 +369,96 @@ regenvc_status regenvc_attn_partial_fwd(const regenvc_tensor *q, const regenvc_t
 {
     return attn_common("regenvc_attn_partial_fwd", q, k_chunk, v_chunk, o_part, REGENVC_F32, lse_part, true, B, H, Sq,
                        Skv_chunk, D, softmax_scale, stream, true);
+}
+
+regenvc_status regenvc_attn_partials_fwd(const regenvc_tensor *q, const regenvc_tensor *k, const regenvc_tensor *v,
+                                         int32_t num_chunks, const int32_t *chunk_start, float *const *o_parts,
+                                         float *const *lse_parts, int32_t B, int32_t H, int32_t Sq, int32_t Skv,
+                                         int32_t D, float softmax_scale, void *stream)
+{
+    const char *fn = "regenvc_attn_partials_fwd";
+    regenvc_status st = check_sizes(B, H, Sq, D);
+    if (st != REGENVC_OK) return st;
+    if ((st = check_scale(softmax_scale)) != REGENVC_OK) return st;
+    if (num_chunks < 1 || num_chunks > REGENVC_MAX_PARTS)
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: num_chunks=%d not in [1, %d]", fn, num_chunks, REGENVC_MAX_PARTS);
+    if (chunk_start == nullptr || o_parts == nullptr || lse_parts == nullptr)
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: chunk_start, o_parts or lse_parts is NULL", fn);
+    if (Skv < 1) return fail(REGENVC_ERR_INVALID_ARG, "%s: key count %d must be >= 1", fn, Skv);
+    if (chunk_start[0] < 0 || chunk_start[num_chunks] > Skv)
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: chunks [%d, %d) lie outside the %d keys", fn, chunk_start[0],
+                    chunk_start[num_chunks], Skv);
+    for (int c = 0; c < num_chunks; ++c) {
+        if (chunk_start[c + 1] <= chunk_start[c])
+            return fail(REGENVC_ERR_INVALID_ARG, "%s: chunk %d = [%d, %d) is empty or reversed", fn, c,
+                        chunk_start[c], chunk_start[c + 1]);
+        if (o_parts[c] == nullptr || lse_parts[c] == nullptr)
+            return fail(REGENVC_ERR_INVALID_ARG, "%s: part %d pointer is NULL", fn, c);
+        if (reinterpret_cast<uintptr_t>(o_parts[c]) % 16 != 0)
+            return fail(REGENVC_ERR_UNSUPPORTED, "%s: o_parts[%d] is not 16-byte aligned", fn, c);
+        if (reinterpret_cast<uintptr_t>(lse_parts[c]) % 4 != 0)
+            return fail(REGENVC_ERR_UNSUPPORTED, "%s: lse_parts[%d] is not 4-byte aligned", fn, c);
+    }
+    if (!q || !k || !v) return fail(REGENVC_ERR_INVALID_ARG, "%s: descriptor is NULL", fn);
+    if (B == 0 || H == 0 || Sq == 0) {
+        g_last_error[0] = '\0';
+        return REGENVC_OK;
+    }
+    Extent ext[3 + 2 * REGENVC_MAX_PARTS];
+    if ((st = check_view("q", q, B, Sq, H, D, 2, &ext[0])) != REGENVC_OK) return st;
+    if ((st = check_view("k", k, B, Skv, H, D, 2, &ext[1])) != REGENVC_OK) return st;
+    if ((st = check_view("v", v, B, Skv, H, D, 2, &ext[2])) != REGENVC_OK) return st;
+    const int64_t rows = (int64_t)B * Sq * H;
+    int n_ext = 3;
+    for (int c = 0; c < num_chunks; ++c) {
+        const Extent eo = flat_extent(o_parts[c], rows * D, 4), el = flat_extent(lse_parts[c], rows, 4);
+        if (overlap(eo, el)) return fail(REGENVC_ERR_INVALID_ARG, "%s: o_parts[%d] overlaps lse_parts[%d]", fn, c, c);
+        for (int i = 0; i < n_ext; ++i)
+            if (overlap(eo, ext[i]) || overlap(el, ext[i]))
+                return fail(REGENVC_ERR_INVALID_ARG, "%s: part %d overlaps an input or another part", fn, c);
+        ext[n_ext++] = eo;
+        ext[n_ext++] = el;
+    }
+    if ((st = check_device()) != REGENVC_OK) return st;
+
+    regenvc::AttnArgs a{};
+    a.q = q->ptr;
+    a.k = k->ptr;
+    a.v = v->ptr;
+    a.q_sb = q->stride_b, a.q_ss = q->stride_s, a.q_sh = q->stride_h;
+    a.k_sb = k->stride_b, a.k_ss = k->stride_s, a.k_sh = k->stride_h;
+    a.v_sb = v->stride_b, a.v_ss = v->stride_s, a.v_sh = v->stride_h;
+    a.o_sb = (int64_t)Sq * H * D, a.o_ss = (int64_t)H * D, a.o_sh = D;  // contiguous partials
+    a.B = B;
+    a.H = H;
+    a.Sq = Sq;
+    a.D = D;
+    a.o_f32 = true;
+    a.scale = softmax_scale;
+    a.kv_off32 = k->stride_s >= 0 && v->stride_s >= 0 && k->stride_s < (1 << 24) && v->stride_s < (1 << 24);
+    if (num_chunks == 1) {  // a plain partial over the one chunk
+        a.k = static_cast<const uint16_t *>(k->ptr) + (int64_t)chunk_start[0] * k->stride_s;
+        a.v = static_cast<const uint16_t *>(v->ptr) + (int64_t)chunk_start[0] * v->stride_s;
+        a.Skv = chunk_start[1] - chunk_start[0];
+        a.o = o_parts[0];
+        a.lse = lse_parts[0];
+    } else {
+        a.n_chunks = num_chunks;
+        a.Skv = chunk_start[num_chunks] - chunk_start[num_chunks - 1];
+        a.o = o_parts[0];
+        a.lse = lse_parts[0];
+        for (int c = 0; c < num_chunks; ++c) {
+            a.ck0[c] = chunk_start[c];
+            a.clen[c] = chunk_start[c + 1] - chunk_start[c];
+            a.co[c] = o_parts[c];
+            a.clse[c] = lse_parts[c];
+        }
+    }
+    regenvc::Workspace ws{};
+    if (g_ws_ptr != nullptr &&
+        (st = bound_workspace(fn, regenvc::attn_workspace_need(a), ext, n_ext, &ws)) != REGENVC_OK)
+        return st;
+    return launched(regenvc::launch_attn(a, static_cast<hipStream_t>(stream), ws), fn);
 }
 
 regenvc_status regenvc_attn_ring_accumulate(const regenvc_tensor *q, const regenvc_tensor *k_chunk,
@@ -567,6 +665,38 @@ regenvc_status regenvc_cross_attn_dual_plan_query(int32_t B, int32_t H, int32_t 
     if (S_img < 1)
         return fail(REGENVC_ERR_INVALID_ARG, "regenvc_cross_attn_dual_plan_query: S_img=%d < 1", S_img);
     return plan_query("regenvc_cross_attn_dual_plan_query", B, H, Sq, S_txt, S_img, D, n_cu, plan);
+}
+
+regenvc_status regenvc_attn_partials_plan_query(int32_t B, int32_t H, int32_t Sq, int32_t num_chunks,
+                                                const int32_t *chunk_start, int32_t D, int32_t n_cu,
+                                                regenvc_attn_plan *plan)
+{
+    const char *fn = "regenvc_attn_partials_plan_query";
+    if (plan == nullptr || chunk_start == nullptr)
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: plan or chunk_start is NULL", fn);
+    if (num_chunks < 1 || num_chunks > REGENVC_MAX_PARTS)
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: num_chunks=%d not in [1, %d]", fn, num_chunks, REGENVC_MAX_PARTS);
+    if (num_chunks == 1) return plan_query(fn, B, H, Sq, chunk_start[1] - chunk_start[0], 0, D, n_cu, plan);
+    if (B < 0 || H < 0 || Sq < 0)
+        return fail(REGENVC_ERR_INVALID_ARG, "%s: negative size (B=%d H=%d Sq=%d)", fn, B, H, Sq);
+    if (n_cu < 1) return fail(REGENVC_ERR_INVALID_ARG, "%s: n_cu=%d < 1", fn, n_cu);
+    if (D != 64 && D != 128) return fail(REGENVC_ERR_UNSUPPORTED, "%s: D=%d not in {64, 128}", fn, D);
+    int32_t clen[REGENVC_MAX_PARTS];
+    for (int c = 0; c < num_chunks; ++c) {
+        clen[c] = chunk_start[c + 1] - chunk_start[c];
+        if (clen[c] < 1) return fail(REGENVC_ERR_INVALID_ARG, "%s: chunk %d is empty or reversed", fn, c);
+    }
+    regenvc::AttnPlan pl{};
+    if (!regenvc::plan_attn_chunks(B, H, Sq, num_chunks, clen, D, n_cu, &pl))
+        return fail(REGENVC_ERR_UNSUPPORTED, "%s: too many query tiles", fn);
+    plan->query_tiles = pl.n_tiles;
+    plan->key_tiles = pl.n_kt;
+    plan->whole_tiles = pl.n_dp;
+    plan->split_tiles = pl.n_tiles - pl.n_dp;
+    plan->key_ranges = pl.n_units > 0 ? pl.seg : 0;
+    plan->workspace_bytes = (int64_t)regenvc::workspace_bytes(pl, D);
+    g_last_error[0] = '\0';
+    return REGENVC_OK;
 }
 
 regenvc_status regenvc_attn_set_workspace(void *workspace, int64_t bytes)

@@ -336,6 +336,35 @@ __device__ __forceinline__ WorkItem work_item(const AttnPlan &pl, int item)
     return w;
 }
 
+// Chunked-partials launches: the chunk of a tile gives its key range (K/V
+// bases moved to the chunk's first key, the chunk length as Skv) and its
+// outputs, and the tile index becomes the one within the chunk.  Other
+// launches pass through unchanged.
+__device__ __forceinline__ AttnArgs chunk_of(const AttnArgs &a, const AttnPlan &pl, int &tile)
+{
+    if (pl.tiles_per_chunk == 0) return a;
+    const int c = tile / pl.tiles_per_chunk;
+    tile -= c * pl.tiles_per_chunk;
+    AttnArgs r = a;
+    r.k = static_cast<const uint16_t *>(a.k) + (int64_t)a.ck0[c] * a.k_ss;
+    r.v = static_cast<const uint16_t *>(a.v) + (int64_t)a.ck0[c] * a.v_ss;
+    r.Skv = a.clen[c];
+    r.o = a.co[c];
+    r.lse = a.clse[c];
+    return r;
+}
+
+// The same for a work item, with the key tiles of its chunk (n_kt) and, for
+// a whole tile, its key range.  A split tile's ranges were planned on the
+// last chunk's key tiles, which every split tile's chunk has.
+__device__ __forceinline__ AttnArgs chunk_view(const AttnArgs &a, const AttnPlan &pl, WorkItem &wi, int &n_kt)
+{
+    const AttnArgs r = chunk_of(a, pl, wi.tile);
+    n_kt = pl.tiles_per_chunk == 0 ? pl.n_kt : (r.Skv + kBlockN - 1) / kBlockN;
+    if (wi.slot < 0) wi.kt1 = n_kt;
+    return r;
+}
+
 // Ring accumulate: how a row's running state (normalized O_run over the key
 // chunks seen so far, and its LSE L_run) and this launch's normalized result
 // (O_c, L_c) combine, by the log-sum-exp identity of the chunk merge:
@@ -587,7 +616,7 @@ __device__ __forceinline__ void wait_vmcnt()
 // bf16 (the precision of a single context-attention output), the second.
 template <int D, bool OUT_F32, bool ACC, bool DUAL = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
+void attn_fwd_kernel(AttnArgs a_in, AttnPlan pl)
 {
     using G = Geo<D>;
     constexpr int NCH = G::NCH, DS = G::DS, DB = G::DB, LOADS = G::LOADS;
@@ -603,7 +632,9 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     const int hi = lane >> 5;   // which half of the wave
     const int col = lane & 31;  // query column owned in the 32x32 accumulators
 
-    const WorkItem wi = work_item(pl, blockIdx.x);
+    WorkItem wi = work_item(pl, blockIdx.x);
+    int n_kt;
+    const AttnArgs a = chunk_view(a_in, pl, wi, n_kt);
     const int tile = wi.tile, slot = wi.slot;
     const int qt = tile % pl.n_qtiles;
     const int bh = tile / pl.n_qtiles;
@@ -617,7 +648,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
     // key/value contexts of this (b, h)
     const KvSrc src0{static_cast<const uint16_t *>(a.k) + b * a.k_sb + h * a.k_sh,
                      static_cast<const uint16_t *>(a.v) + b * a.v_sb + h * a.v_sh,
-                     a.k_ss, a.v_ss, a.Skv, pl.n_kt, a.kv_off32};
+                     a.k_ss, a.v_ss, a.Skv, n_kt, a.kv_off32};
 
     // Q^T operand fragments stay in registers for the whole key loop.
     bf16x8 qf[DS];
@@ -1061,7 +1092,7 @@ void attn_fwd_kernel(AttnArgs a, AttnPlan pl)
 // kSpecLimit), and the same running sum.
 template <int D, bool OUT_F32, bool ACC>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
+void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
 {
     using G = Geo<D, kStagesPP>;
     constexpr int NCH = G::NCH, LOADS = G::LOADS;
@@ -1080,7 +1111,9 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     const int g = lane >> 4;   // lane group: 4 keys of each 16-key block, 4 dims of each 16-dim block
     const int x = lane & 15;   // query column within a 16-query block
 
-    const WorkItem wi = work_item(pl, blockIdx.x);
+    WorkItem wi = work_item(pl, blockIdx.x);
+    int n_kt;
+    const AttnArgs a = chunk_view(a_in, pl, wi, n_kt);
     const int tile = wi.tile, kt0 = wi.kt0, kt1 = wi.kt1, slot = wi.slot;
     const int qt = tile % pl.n_qtiles;
     const int bh = tile / pl.n_qtiles;
@@ -1095,7 +1128,7 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
     const uint16_t *vp = static_cast<const uint16_t *>(a.v) + b * a.v_sb + h * a.v_sh;
     const int Skv = a.Skv;
     const int T = kt1 - kt0;  // key tiles of this work item, >= 1
-    const bool ragged_end = kt1 == pl.n_kt && (Skv % kBlockN) != 0;
+    const bool ragged_end = kt1 == n_kt && (Skv % kBlockN) != 0;
 
     // Q^T operand fragments (B of S^T = K Q^T): query block qb, dims
     // 32*ks + 8*g .. +7 of query qb*16 + x.
@@ -1509,18 +1542,19 @@ void attn_fwd_pingpong_kernel(AttnArgs a, AttnPlan pl)
 // issued before any of them is used, combined online (running max, sum and
 // weighted O), so the loop is not a chain of dependent memory accesses.
 template <bool OUT_F32>
-__global__ __launch_bounds__(256) void split_fixup_kernel(AttnArgs a, AttnPlan pl)
+__global__ __launch_bounds__(256) void split_fixup_kernel(AttnArgs a_in, AttnPlan pl)
 {
     constexpr int BM = kWaves * 32;
     constexpr int FB = 8;
-    const int per_row = a.D / 4;
+    const int per_row = a_in.D / 4;
     const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t rows = (int64_t)(pl.n_tiles - pl.n_dp) * BM;
     const int64_t row = gid / per_row;
     if (row >= rows) return;
     const int d = (int)(gid % per_row) * 4;
     const int j = (int)(row / BM), r = (int)(row % BM);
-    const int tile = pl.n_dp + j;
+    int tile = pl.n_dp + j;
+    const AttnArgs a = chunk_of(a_in, pl, tile);
     const int qt = tile % pl.n_qtiles;
     const int bh = tile / pl.n_qtiles;
     const int h = bh % a.H, b = bh / a.H;
@@ -1712,14 +1746,21 @@ int forced_schedule()
     return 0;
 }
 
+// The work plan of launch `a` on n_cu compute units.
+bool plan_for(const AttnArgs &a, int n_cu, AttnPlan *pl)
+{
+    if (a.n_chunks > 1) return plan_attn_chunks(a.B, a.H, a.Sq, a.n_chunks, a.clen, a.D, n_cu, pl);
+    return plan_attn(a.B, a.H, a.Sq, a.Skv, a.D, n_cu, pl, a.k2 != nullptr ? a.Skv2 : 0);
+}
+
 template <int D, bool OUT_F32>
 hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream, const Workspace &given)
 {
     constexpr int BM = kWaves * 32;
     AttnPlan pl{};
     if (OUT_F32 && a.k2 != nullptr) return hipErrorInvalidValue;  // dual context: bf16 output only
-    if (!plan_attn(a.B, a.H, a.Sq, a.Skv, D, cu_count(), &pl, a.k2 != nullptr ? a.Skv2 : 0))
-        return hipErrorInvalidConfiguration;
+    if (a.n_chunks > 1 && (!OUT_F32 || a.k2 != nullptr || a.run_lse != nullptr)) return hipErrorInvalidValue;
+    if (!plan_for(a, cu_count(), &pl)) return hipErrorInvalidConfiguration;
     void *ws = nullptr;     // pool allocation to return
     if (pl.n_units > 0) {
         const size_t bytes = workspace_bytes(pl, D);
@@ -1786,6 +1827,32 @@ bool plan_attn(int B, int H, int Sq, int Skv, int D, int n_cu, AttnPlan *out, in
     return true;
 }
 
+bool plan_attn_chunks(int B, int H, int Sq, int n_chunks, const int32_t *clen, int D, int n_cu, AttnPlan *out)
+{
+    constexpr int BM = kWaves * 32;
+    if (n_chunks < 1 || n_chunks > kMaxChunks || B < 0 || H < 0 || Sq < 0 || n_cu < 1) return false;
+    for (int c = 0; c < n_chunks; ++c)
+        if (clen[c] < 1) return false;
+    const int64_t n_qtiles = ((int64_t)Sq + BM - 1) / BM;
+    const int64_t per_chunk = n_qtiles * H * B;
+    if (n_qtiles * H > 0x7fffffff || per_chunk > 0x7fffffff / n_chunks) return false;
+    auto kt = [](int len) { return (int)(((int64_t)len + kBlockN - 1) / kBlockN); };
+    const int n_kt = kt(clen[n_chunks - 1]);
+    *out = make_plan((int)n_qtiles, (int)(per_chunk * n_chunks), n_kt, n_cu, D);
+    out->tiles_per_chunk = (int)per_chunk;
+    if (out->n_units > 0 && per_chunk > 0) {
+        // the split tiles are the last ones: their chunks must all have n_kt key tiles
+        for (int c = (int)(out->n_dp / per_chunk); c < n_chunks; ++c)
+            if (kt(clen[c]) != n_kt) {
+                out->n_dp = out->n_tiles;
+                out->seg = 1;
+                out->n_units = 0;
+                break;
+            }
+    }
+    return true;
+}
+
 size_t workspace_bytes(const AttnPlan &pl, int D)
 {
     return (size_t)pl.n_units * (kWaves * 32) * (D + 1) * sizeof(float);
@@ -1799,7 +1866,7 @@ int device_cu_count()
 size_t attn_workspace_need(const AttnArgs &a)
 {
     AttnPlan pl{};
-    if (!plan_attn(a.B, a.H, a.Sq, a.Skv, a.D, cu_count(), &pl, a.k2 != nullptr ? a.Skv2 : 0)) return 0;
+    if (!plan_for(a, cu_count(), &pl)) return 0;
     return workspace_bytes(pl, a.D);
 }
 

@@ -6,6 +6,8 @@
 
 namespace regenvc {
 
+constexpr int kMaxChunks = 16;  // key chunks of one chunked-partials launch
+
 // One attention launch: Q [B,Sq,H,D], K/V [B,Skv,H,D] (bf16, element strides,
 // d contiguous); O [B,Sq,H,D] bf16 or f32; optional f32 LSE [B,H,Sq].
 struct AttnArgs {
@@ -39,6 +41,14 @@ struct AttnArgs {
     int64_t v2_sb, v2_ss, v2_sh;
     int32_t Skv2;
     bool kv2_off32;
+    // Chunked partials (n_chunks > 1): the launch covers n_chunks key chunks
+    // at once; query tile t belongs to chunk c = t / (tiles per chunk),
+    // attends over keys [ck0[c], ck0[c] + clen[c]) of k/v and writes its
+    // normalized partial to co[c] (f32, strides o_*) and its LSE to clse[c].
+    int32_t n_chunks;
+    int32_t ck0[kMaxChunks], clen[kMaxChunks];
+    float *co[kMaxChunks];
+    float *clse[kMaxChunks];
 };
 
 // Work plan of one attention launch.  Query tiles [0, n_dp) are processed
@@ -58,6 +68,7 @@ struct AttnPlan {
     int32_t n_units;   // (n_tiles - n_dp) * (seg + seg2)
     int32_t n_kt2;     // key tiles of the second context (dual launches; else 0)
     int32_t seg2;      // key ranges of a split tile over the second context (else 0)
+    int32_t tiles_per_chunk;  // chunked partials: B * H * n_qtiles (else 0); n_kt is the last chunk's
     float *ws_o;       // [n_units][query tile rows][D] partial O (normalized)
     float *ws_lse;     // [n_units][query tile rows] partial LSE
 };
@@ -98,6 +109,10 @@ struct NormRopeArgs {
 // Work plan of an attention launch of this shape on n_cu compute units
 // (host-only); false if the shape has no valid plan (Skv < 1, too many tiles).
 bool plan_attn(int B, int H, int Sq, int Skv, int D, int n_cu, AttnPlan *out, int Skv2 = 0);
+// The same for a chunked-partials launch over n_chunks chunks of clen[c]
+// keys (each >= 1): tiles are split only where every split tile's chunk has
+// the last chunk's key tile count.
+bool plan_attn_chunks(int B, int H, int Sq, int n_chunks, const int32_t *clen, int D, int n_cu, AttnPlan *out);
 // Bytes of split-tile partials a plan needs (0 when nothing is split).
 size_t workspace_bytes(const AttnPlan &pl, int D);
 // Compute units of the current device (cached per device).

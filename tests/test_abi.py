@@ -281,3 +281,74 @@ def test_dual_plan_query(lib):
 
 def test_pool_draws_is_host_only(lib):
     assert lib.regenvc_attn_pool_draws() >= 0
+
+
+def partials(lib, bounds=(0, 32, 64), parts=None, lparts=None, q=None, k=None, v=None, B=1, H=2, Sq=64, Skv=64,
+             D=128, scale=0.088):
+    n = len(bounds) - 1
+    q = q if q is not None else T(FAKE, S=Sq, H=H, D=D)
+    k = k if k is not None else T(FAKE + 0x1000000, S=Skv, H=H, D=D)
+    v = v if v is not None else T(FAKE + 0x2000000, S=Skv, H=H, D=D)
+    parts = parts if parts is not None else [FAKE + 0x5000000 + i * 0x1000000 for i in range(max(n, 0))]
+    lparts = lparts if lparts is not None else [FAKE + 0x20000000 + i * 0x100000 for i in range(max(n, 0))]
+    ba = (ctypes.c_int32 * max(len(bounds), 1))(*bounds)
+    pa = (ctypes.c_void_p * max(len(parts), 1))(*parts)
+    la = (ctypes.c_void_p * max(len(lparts), 1))(*lparts)
+    return lib.regenvc_attn_partials_fwd(ctypes.byref(q), ctypes.byref(k), ctypes.byref(v), n, ba, pa, la, B, H, Sq,
+                                         Skv, D, scale, None)
+
+
+def test_chunked_partials_validation(lib):
+    """regenvc_attn_partials_fwd checks its chunks and part pointers before
+    any HIP call."""
+    expect(lib, partials(lib, bounds=(0,)), _lib.ERR_INVALID_ARG, "num_chunks")
+    expect(lib, partials(lib, bounds=tuple(range(18)), Skv=64), _lib.ERR_INVALID_ARG, "num_chunks")
+    expect(lib, partials(lib, bounds=(0, 32, 32, 64)), _lib.ERR_INVALID_ARG, "empty")
+    expect(lib, partials(lib, bounds=(0, 40, 20)), _lib.ERR_INVALID_ARG, "empty or reversed")
+    expect(lib, partials(lib, bounds=(-1, 32, 64)), _lib.ERR_INVALID_ARG, "outside")
+    expect(lib, partials(lib, bounds=(0, 32, 65)), _lib.ERR_INVALID_ARG, "outside")
+    expect(lib, partials(lib, Skv=0, bounds=(0, 0, 0)), _lib.ERR_INVALID_ARG, "key count")
+    expect(lib, partials(lib, parts=[FAKE + 0x5000000, 0]), _lib.ERR_INVALID_ARG, "NULL")
+    expect(lib, partials(lib, parts=[FAKE + 0x5000008, FAKE + 0x6000000]), _lib.ERR_UNSUPPORTED, "aligned")
+    expect(lib, partials(lib, lparts=[FAKE + 0x20000002, FAKE + 0x20100000]), _lib.ERR_UNSUPPORTED, "aligned")
+    expect(lib, partials(lib, parts=[FAKE + 0x5000000, FAKE + 0x5000000 + 1024]), _lib.ERR_INVALID_ARG,
+           "another part")
+    expect(lib, partials(lib, parts=[FAKE + 0x1000000, FAKE + 0x6000000]), _lib.ERR_INVALID_ARG, "overlaps")
+    expect(lib, partials(lib, D=96), _lib.ERR_UNSUPPORTED, "head dim")
+    expect(lib, partials(lib, scale=float("nan")), _lib.ERR_INVALID_ARG, "finite")
+    expect(lib, partials(lib, B=0), _lib.OK)
+
+
+@pytest.mark.skipif(has_gpu_node(), reason="would reach a launch on fake addresses on a GPU machine")
+def test_chunked_partials_valid_arguments_reach_the_device_check(lib):
+    expect(lib, partials(lib, bounds=(3, 30, 64)), _lib.ERR_HIP, "hip")
+
+
+def test_chunked_partials_plan_query(lib):
+    """The rank share (H=5, 10920 queries, 4 chunks of 2730) in one launch:
+    860 query tiles, 3 whole rounds on 256 CUs, the 92 leftover tiles (all in
+    the last chunk) split into key ranges.  With chunks of different key tile
+    counts under the split tiles, nothing is split."""
+    plan = _lib.AttnPlan()
+    b = (ctypes.c_int32 * 5)(0, 2730, 5460, 8190, 10920)
+    expect(lib, lib.regenvc_attn_partials_plan_query(1, 5, 10920, 4, b, 128, 256, ctypes.byref(plan)), _lib.OK)
+    assert plan.query_tiles == 860 and plan.key_tiles == 43
+    assert plan.whole_tiles == 768 and plan.split_tiles == 92 and plan.key_ranges >= 2
+    assert plan.workspace_bytes == plan.split_tiles * plan.key_ranges * 256 * 129 * 4
+    # 72 tiles on 256 CUs: every tile is a split candidate, and chunk 0 has 1 key tile against 6
+    b = (ctypes.c_int32 * 5)(5, 69, 70, 400, 777)
+    expect(lib, lib.regenvc_attn_partials_plan_query(2, 3, 700, 4, b, 128, 256, ctypes.byref(plan)), _lib.OK)
+    assert plan.query_tiles == 72 and plan.split_tiles == 0 and plan.workspace_bytes == 0
+    # equal key tile counts: the same tiles are split
+    b = (ctypes.c_int32 * 4)(0, 3000, 6000, 9000)
+    expect(lib, lib.regenvc_attn_partials_plan_query(1, 2, 1000, 3, b, 128, 256, ctypes.byref(plan)), _lib.OK)
+    assert plan.query_tiles == 24 and plan.split_tiles > 0 and plan.key_ranges >= 2
+    # one chunk: the plain partial's plan
+    b = (ctypes.c_int32 * 2)(100, 2830)
+    p1 = _lib.AttnPlan()
+    expect(lib, lib.regenvc_attn_partials_plan_query(1, 5, 10920, 1, b, 128, 256, ctypes.byref(plan)), _lib.OK)
+    expect(lib, lib.regenvc_attn_plan_query(1, 5, 10920, 2730, 128, 256, ctypes.byref(p1)), _lib.OK)
+    assert {f: getattr(plan, f) for f, _ in plan._fields_} == {f: getattr(p1, f) for f, _ in p1._fields_}
+    b = (ctypes.c_int32 * 3)(0, 10, 10)
+    expect(lib, lib.regenvc_attn_partials_plan_query(1, 5, 10920, 2, b, 128, 256, ctypes.byref(plan)),
+           _lib.ERR_INVALID_ARG, "empty")
