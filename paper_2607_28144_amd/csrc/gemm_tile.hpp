@@ -78,17 +78,23 @@ __device__ __forceinline__ int swz(int row, int chunk)
     return chunk ^ ((row >> 1) & 7);
 }
 
+// Activations of the epilogues, in the sigmoid form with the hardware
+// base-2 exponential and reciprocal (both within an ulp or two of fp32,
+// far below the bf16 rounding that follows): no fp32 division.
+//   gelu_tanh(x) = x/2 (1 + tanh(u)) = x sigmoid(2u),  u = sqrt(2/pi) (x + 0.044715 x^3),
+//   sigmoid(2u) = 1 / (1 + 2^z),  z = -2 log2(e) u = x (kG1 + kG3 x^2).
 __device__ __forceinline__ float gelu_tanh(float x)
 {
-    // x/2 (1 + tanh(u)), tanh(u) = 1 - 2 / (e^(2u) + 1); u = sqrt(2/pi) (x + 0.044715 x^3)
-    const float u = 0.7978845608028654f * fmaf(0.044715f * x, x * x, x);
-    const float t = 1.0f - 2.0f / (__expf(2.0f * u) + 1.0f);
-    return 0.5f * x * (1.0f + t);
+    constexpr float kG1 = -2.0f * 1.4426950408889634f * 0.7978845608028654f;
+    constexpr float kG3 = kG1 * 0.044715f;
+    const float z = x * fmaf(kG3, x * x, kG1);
+    return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z));
 }
 
+// silu(x) = x sigmoid(x) = x / (1 + 2^(-x log2 e)).
 __device__ __forceinline__ float silu(float x)
 {
-    return x / (1.0f + __expf(-x));
+    return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * x));
 }
 
 __device__ __forceinline__ float bf(uint16_t b)
