@@ -61,13 +61,30 @@ regenvc_status regenvc_vae_split(int32_t H, int32_t W, int32_t ty, int32_t tx, i
      w: bf16 [Cout, 3, 3, 3, Cin]; bias: bf16 [Cout]; silu != 0 applies SiLU
      out: bf16 [n_tiles][T][Hr][Wr][Cout]; a tile's values at rows >=
           region height or columns >= region width are unspecified
+     workspace: NULL, or caller-owned DEVICE memory of workspace_bytes
+          (256-byte aligned, not overlapping any other argument) for the
+          split-K form: when the output tiles would leave most compute units
+          idle (one GPU's single tile), K is cut into ranges whose f32
+          partial sums go to the workspace and a second kernel adds them,
+          the bias and the activation.  Up to
+          regenvc_vae_conv3d_workspace bytes are used; less gives fewer
+          ranges, NULL (or too little for two) none.  The result is the same
+          up to fp32 summation order.  Nothing is allocated.
    Cin, Cout multiples of 64; T >= 1; 1 <= n_tiles <= REGENVC_VAE_MAX_TILES;
    every region inside the plane, no larger than Hr x Wr; pointers 16-byte
    aligned; out must not overlap in, w or bias. */
 regenvc_status regenvc_vae_conv3d_fwd(const void *in, int32_t in_is_plane, const void *w, const void *bias,
                                       int32_t silu, void *out, int32_t T, int32_t H, int32_t W, int32_t Cin,
                                       int32_t Cout, const regenvc_vae_tile *tiles, int32_t n_tiles,
-                                      int32_t Hr, int32_t Wr, void *stream);
+                                      int32_t Hr, int32_t Wr, void *workspace, int64_t workspace_bytes,
+                                      void *stream);
+
+/* Workspace bytes that let regenvc_vae_conv3d_fwd of this shape use its
+   full split-K form on a device with n_cu compute units (0: it does not
+   split).  Host-only; T, Hr, Wr, n_tiles >= 1, Cin and Cout multiples of
+   64, n_cu >= 1. */
+regenvc_status regenvc_vae_conv3d_workspace(int32_t T, int32_t Hr, int32_t Wr, int32_t n_tiles, int32_t Cin,
+                                            int32_t Cout, int32_t n_cu, int64_t *bytes);
 
 /* Blended gather: out (bf16 [T, H, W, C]) = sum over the tiles covering each
    pixel of ramp_row x ramp_col x tile value, from the tiles' outputs bf16

@@ -83,7 +83,9 @@ _SIGNATURES = {
     "regenvc_vae_split": [_i32, _i32, _i32, _i32, _i32, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32),
                           ctypes.POINTER(ctypes.c_int32)],
     "regenvc_vae_conv3d_fwd": [ctypes.c_void_p, _i32, ctypes.c_void_p, ctypes.c_void_p, _i32, ctypes.c_void_p,
-                               _i32, _i32, _i32, _i32, _i32, ctypes.c_void_p, _i32, _i32, _i32, ctypes.c_void_p],
+                               _i32, _i32, _i32, _i32, _i32, ctypes.c_void_p, _i32, _i32, _i32, ctypes.c_void_p,
+                               ctypes.c_int64, ctypes.c_void_p],
+    "regenvc_vae_conv3d_workspace": [_i32, _i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_int64)],
     "regenvc_vae_blend": [ctypes.c_void_p, ctypes.c_void_p, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32,
                           ctypes.c_void_p, ctypes.c_void_p],
     "regenvc_dit_block_workspace": [_i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_int64)],

@@ -2,9 +2,9 @@
 // block (dense rows) and the VAE's causal 3D convolution (rows gathered as
 // an implicit GEMM): out[m][n] = epilogue(sum_k A[m][k] W[n][k]).
 //
-// Workgroup = 8 waves (two per SIMD) = one BM x BN output tile, BN = 64 WN;
-// the waves form an (8 / WN) x WN grid, each owning (BM / (8 / WN)) rows x
-// 64 channels on v_mfma_f32_16x16x32_bf16.  The product is formed
+// Workgroup = 8 waves (two per SIMD) = one BM x BN output tile, BN = 16 NB
+// WN; the waves form an (8 / WN) x WN grid, each owning (BM / (8 / WN)) rows
+// x 16 NB channels on v_mfma_f32_16x16x32_bf16.  The product is formed
 // transposed, C^T = W A^T, so that a lane's accumulator holds four
 // consecutive output channels of one row (what the epilogues want).  K
 // advances in steps of 64: both operand tiles go HBM -> LDS with
@@ -43,6 +43,7 @@ enum Epi : int32_t {
     kBiasGelu = 1,    // out bf16 = gelu_tanh(y + bias)
     kGatedRes = 2,    // out f32 (in place) = out + gate[n] * (y + bias[n])   (gate may be null: 1)
     kBiasSilu = 3,    // out bf16 = silu(y + bias)
+    kPartial = 4,     // out f32 = y over this workgroup's share of K (split-K partial, no bias)
 };
 
 // Output side of a tile launch.
@@ -53,6 +54,7 @@ struct Out {
     void *out;            // bf16 or f32 [M, N], row stride ldo
     int64_t ldo;
     int32_t M, N, K;
+    int32_t splits;       // kPartial: K split into this many contiguous ranges, one per launch slice
 };
 
 #pragma clang diagnostic push
@@ -102,14 +104,17 @@ __device__ __forceinline__ float bf(uint16_t b)
     return __uint_as_float(((uint32_t)b) << 16);
 }
 
-template <int BM, int WN, int EPI, class ASrc>
+// One BM x BN output tile.  The launch has n_tiles workgroups per K slice;
+// with EPI == kPartial it has o.splits slices (workgroup s * n_tiles + t:
+// tile t over the s-th of o.splits contiguous ranges of K steps), each
+// writing its partial sums to its own f32 [M][ldo] plane of o.out.
+template <int BM, int WN, int EPI, class ASrc, int NB = 4>
 __device__ __forceinline__ void tile_body(const ASrc &asrc, const Out &o, int tiles_n, int n_tiles, char *smem)
 {
-    constexpr int BN = 64 * WN;
+    constexpr int BN = 16 * NB * WN;     // NB 16-channel MFMA blocks per wave across
     constexpr int WGM = kWaves / WN;     // waves along M
     constexpr int WM = BM / WGM;         // rows per wave
     constexpr int MB = WM / 16;          // 16-row MFMA blocks per wave
-    constexpr int NB = 4;                // 16-channel MFMA blocks per wave
     constexpr int A_BYTES = BM * kRowBytes;
     constexpr int W_BYTES = BN * kRowBytes;
     constexpr int STAGE = A_BYTES + W_BYTES;
@@ -130,7 +135,9 @@ __device__ __forceinline__ void tile_body(const ASrc &asrc, const Out &o, int ti
     // resident on an XCD at a time cover about 4 row blocks x 8 channel
     // blocks: each A row block and W block they read serves several of them
     // from the XCD's L2.
-    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int sp = EPI == kPartial ? (int)blockIdx.x / n_tiles : 0;  // K slice
+    const int bid = EPI == kPartial ? (int)blockIdx.x - sp * n_tiles : (int)blockIdx.x;
+    const int xcd = bid & 7, slot = bid >> 3;
     const int tile = xcd * (n_tiles >> 3) + min(xcd, n_tiles & 7) + slot;
     const int tiles_m = n_tiles / tiles_n;
     const int group = tile / (kGroupM * tiles_n), in_group = tile - group * kGroupM * tiles_n;
@@ -174,10 +181,12 @@ __device__ __forceinline__ void tile_body(const ASrc &asrc, const Out &o, int ti
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int nk = o.K / kBK;
-    issue(0, 0);
-    for (int kt = 0; kt < nk; ++kt) {
-        const int st = kt & 1;
+    const int nk_all = o.K / kBK;
+    const int k_begin = EPI == kPartial ? (int)((int64_t)sp * nk_all / o.splits) : 0;
+    const int nk = EPI == kPartial ? (int)((int64_t)(sp + 1) * nk_all / o.splits) : nk_all;
+    issue(k_begin, 0);
+    for (int kt = k_begin; kt < nk; ++kt) {
+        const int st = (kt - k_begin) & 1;
         wait_all_copies();   // this wave's copies of step kt landed
         __syncthreads();     // ... and every wave's; step kt-1's stage is free
         if (kt + 1 < nk) issue(kt + 1, st ^ 1);
@@ -192,7 +201,7 @@ __device__ __forceinline__ void tile_body(const ASrc &asrc, const Out &o, int ti
             return *(const lds_bf16x8 *)(sa + r * kRowBytes + swz(r, (s / MB) * 4 + g) * 16);
         };
         auto wfrag = [&](int ks, int nb) {
-            const int r = wn * 64 + nb * 16 + x;
+            const int r = wn * (16 * NB) + nb * 16 + x;
             return *(const lds_bf16x8 *)(sw + r * kRowBytes + swz(r, ks * 4 + g) * 16);
         };
         bf16x8 wf[2][NB], ar[3];
@@ -216,10 +225,10 @@ __device__ __forceinline__ void tile_body(const ASrc &asrc, const Out &o, int ti
         }
     }
 
-    // epilogue: acc[nb][mb][i] = y[m0 + wm*WM + mb*16 + x][n0 + wn*64 + nb*16 + 4g + i]
+    // epilogue: acc[nb][mb][i] = y[m0 + wm*WM + mb*16 + x][n0 + wn*16*NB + nb*16 + 4g + i]
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-        const int n = n0 + wn * 64 + nb * 16 + 4 * g;
+        const int n = n0 + wn * (16 * NB) + nb * 16 + 4 * g;
         if (n >= o.N) continue;
         f32x4 bv = {0.f, 0.f, 0.f, 0.f};
         if (o.bias != nullptr) {
@@ -234,7 +243,10 @@ __device__ __forceinline__ void tile_body(const ASrc &asrc, const Out &o, int ti
             const int m = m0 + wm * WM + mb * 16 + x;
             if (m >= o.M) continue;
             const f32x4 y = acc[nb][mb] + bv;
-            if constexpr (EPI == kGatedRes) {
+            if constexpr (EPI == kPartial) {
+                *reinterpret_cast<f32x4 *>(static_cast<float *>(o.out) + ((int64_t)sp * o.M + m) * o.ldo + n) =
+                    acc[nb][mb];
+            } else if constexpr (EPI == kGatedRes) {
                 f32x4 *p = reinterpret_cast<f32x4 *>(static_cast<float *>(o.out) + (int64_t)m * o.ldo + n);
                 *p = *p + gv * y;
             } else {
@@ -248,11 +260,11 @@ __device__ __forceinline__ void tile_body(const ASrc &asrc, const Out &o, int ti
     }
 }
 
-// LDS bytes of a BM x BN tile's double-buffered ring.
-template <int BM, int WN>
+// LDS bytes of a BM x (16 NB WN) tile's double-buffered ring.
+template <int BM, int WN, int NB = 4>
 constexpr int lds_bytes()
 {
-    return 2 * (BM + 64 * WN) * kRowBytes;
+    return 2 * (BM + 16 * NB * WN) * kRowBytes;
 }
 
 // XCD-aware tile count helpers for the launchers.

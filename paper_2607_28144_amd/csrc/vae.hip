@@ -10,14 +10,19 @@
 // contiguous run of Cin values, so a K step of 64 channels of one tap is
 // one 128-byte row per pixel, copied HBM -> LDS like a dense row; a tap
 // that falls before the first frame or outside the tile's region is copied
-// from a page of zeros instead (the zero padding).  Tiles of 128 output
-// channels (Cout = 384 splits into three), 128 or 256 pixel rows by how the
-// tiles fill the compute units.
+// from a page of zeros instead (the zero padding).  Tiles of 128 pixel
+// rows x 384 output channels; when they are too few to fill the compute
+// units (one GPU's single tile), K is split into ranges whose f32 partial
+// sums a second kernel adds, with the bias and the activation.
 //
 // Blend: one thread per (pixel, 8 channels) walks the tiles whose region
 // covers the pixel and adds weight x value, the weight the product of the
 // two axes' ramps (fp32).  HBM-bound.
 #include "vae_kernels.hpp"
+
+#include <stdint.h>
+
+#include <algorithm>
 
 #include "gemm_tile.hpp"
 
@@ -30,7 +35,15 @@ namespace {
 
 using tile::kBK;
 using tile::kThreads;
+
+// Output tile of the convolution: 128 rows x 384 channels (all of Cout up to
+// 384: each gathered A row block is read once for every output channel);
+// waves 2 x 4, each 64 rows x 96 channels.
+constexpr int kConvBM = 128;
+constexpr int kConvNB = 6;
+constexpr int kConvBN = 16 * kConvNB * 4;
 typedef tile::bf16x8 bf16x8;
+typedef tile::f32x4 f32x4;
 
 // A rows of the convolution: pixel m of the listed tiles' regions, K step kt
 // = tap kt / (Cin / 64), channels 64 (kt % (Cin / 64)) .. +63.  A row keeps
@@ -78,16 +91,47 @@ struct ConvA {
     }
 };
 
+// EPI == kPartial: split-K, f32 partial sums of `splits` K ranges into the
+// workspace (bias and activation follow in vae_reduce_kernel).
 template <int BM, int EPI>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void conv3d_kernel(ConvArgs a, int tiles_n, int n_tiles)
+void conv3d_kernel(ConvArgs a, int tiles_n, int n_tiles, int splits)
 {
-    __shared__ __attribute__((aligned(1024))) char smem[tile::lds_bytes<BM, 2>()];
+    __shared__ __attribute__((aligned(1024))) char smem[tile::lds_bytes<BM, 4, kConvNB>()];
     const ConvA src{static_cast<const uint16_t *>(a.in), &a, a.Cin / kBK,
                     a.in_is_plane ? (int64_t)a.H * a.W : (int64_t)a.Hr * a.Wr, a.in_is_plane ? a.W : a.Wr};
-    const tile::Out o{static_cast<const uint16_t *>(a.w), static_cast<const uint16_t *>(a.bias), nullptr, a.out,
-                      a.Cout, a.n_tiles * a.T * a.Hr * a.Wr, a.Cout, 27 * a.Cin};
-    tile::tile_body<BM, 2, EPI>(src, o, tiles_n, n_tiles, smem);
+    const bool part = EPI == tile::kPartial;
+    const tile::Out o{static_cast<const uint16_t *>(a.w), part ? nullptr : static_cast<const uint16_t *>(a.bias),
+                      nullptr, part ? a.ws : a.out, a.Cout, a.n_tiles * a.T * a.Hr * a.Wr, a.Cout, 27 * a.Cin, splits};
+    tile::tile_body<BM, 4, EPI, ConvA, kConvNB>(src, o, tiles_n, n_tiles, smem);
+}
+
+// Sum of the split-K partials, bias and activation: one thread per 8
+// channels of one output row.
+template <bool SILU>
+__global__ __launch_bounds__(256) void vae_reduce_kernel(ConvArgs a, int splits)
+{
+    const int64_t M = (int64_t)a.n_tiles * a.T * a.Hr * a.Wr;
+    const int cg = a.Cout / 8;
+    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (gid >= M * cg) return;
+    const int64_t m = gid / cg;
+    const int c = (int)(gid - m * cg) * 8;
+    const float *p = static_cast<const float *>(a.ws) + m * a.Cout + c;
+    f32x4 s0 = *reinterpret_cast<const f32x4 *>(p), s1 = *reinterpret_cast<const f32x4 *>(p + 4);
+    for (int k = 1; k < splits; ++k) {
+        const float *q = p + (int64_t)k * M * a.Cout;
+        s0 += *reinterpret_cast<const f32x4 *>(q);
+        s1 += *reinterpret_cast<const f32x4 *>(q + 4);
+    }
+    const bf16x8 bb = *reinterpret_cast<const bf16x8 *>(static_cast<const uint16_t *>(a.bias) + c);
+    bf16x8 o;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float y = (e < 4 ? s0[e] : s1[e - 4]) + (float)bb[e];
+        o[e] = (__bf16)(SILU ? tile::silu(y) : y);
+    }
+    *reinterpret_cast<bf16x8 *>(static_cast<uint16_t *>(a.out) + m * a.Cout + c) = o;
 }
 
 __device__ __forceinline__ float ramp(int p, int c0, int c1, int n, int band)
@@ -129,18 +173,30 @@ __global__ __launch_bounds__(256) void vae_blend_kernel(BlendArgs a)
     *reinterpret_cast<bf16x8 *>(static_cast<uint16_t *>(a.out) + (((int64_t)t * a.H + y) * a.W + x) * a.C + c) = o;
 }
 
-template <int BM>
-hipError_t launch_conv_bm(const ConvArgs &a, hipStream_t stream)
+hipError_t launch_conv(const ConvArgs &a, int splits, hipStream_t stream)
 {
+    constexpr int BM = kConvBM;
     const int64_t M = (int64_t)a.n_tiles * a.T * a.Hr * a.Wr;
-    const int tiles_n = tile::tiles_along(a.Cout, 128);
+    const int tiles_n = tile::tiles_along(a.Cout, kConvBN);
     const int n_tiles = (int)((M + BM - 1) / BM) * tiles_n;
-    if (a.silu)
+    if (splits > 1) {
+        hipLaunchKernelGGL((conv3d_kernel<BM, tile::kPartial>), dim3((unsigned)(n_tiles * splits)), dim3(kThreads), 0,
+                           stream, a, tiles_n, n_tiles, splits);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const int64_t n = M * (a.Cout / 8);
+        const dim3 grid((unsigned)((n + 255) / 256));
+        if (a.silu)
+            hipLaunchKernelGGL(vae_reduce_kernel<true>, grid, dim3(256), 0, stream, a, splits);
+        else
+            hipLaunchKernelGGL(vae_reduce_kernel<false>, grid, dim3(256), 0, stream, a, splits);
+    } else if (a.silu) {
         hipLaunchKernelGGL((conv3d_kernel<BM, tile::kBiasSilu>), dim3((unsigned)n_tiles), dim3(kThreads), 0, stream,
-                           a, tiles_n, n_tiles);
-    else
+                           a, tiles_n, n_tiles, 1);
+    } else {
         hipLaunchKernelGGL((conv3d_kernel<BM, tile::kBias>), dim3((unsigned)n_tiles), dim3(kThreads), 0, stream, a,
-                           tiles_n, n_tiles);
+                           tiles_n, n_tiles, 1);
+    }
     return hipGetLastError();
 }
 
@@ -154,26 +210,35 @@ int cu_count_here()
 
 }  // namespace
 
-// Rounds of tiles over the CUs, each tile costing its rows: the smaller
-// 128-row tile wins when the 256-row tiles would leave CUs idle (one split
-// VAE tile of the window is ~8k pixels x 3 channel blocks: 96 tiles of 256
-// rows for 256 CUs).
-int conv_tile_rows(int64_t M, int N, int n_cu)
+// Split-K when the output tiles (128 rows x all channels) leave more than
+// half the compute units idle: K (27 taps x Cin) cut into as many ranges as
+// fill the CUs in one round (at most 8), limited by the workspace (one f32
+// copy of the output per range).  One split VAE tile of the window (8092
+// pixels: 64 row tiles) runs as 64 x 4 workgroups.
+int conv_splits(int64_t M, int N, int Cin, int n_cu, int64_t ws_bytes)
 {
-    const int64_t tn = (N + 127) / 128;
-    auto cost = [&](int bm) {
-        const int64_t tiles = (M + bm - 1) / bm * tn;
-        return (double)((tiles + n_cu - 1) / n_cu) * bm;
-    };
-    return cost(128) < cost(256) ? 128 : 256;
+    const int64_t tiles = (M + kConvBM - 1) / kConvBM * ((N + kConvBN - 1) / kConvBN);
+    const int nk = 27 * Cin / kBK;
+    if (tiles * 2 > n_cu) return 1;
+    int s = (int)std::min<int64_t>(8, n_cu / tiles);
+    s = std::min(s, nk);
+    const int64_t plane = M * N * (int64_t)sizeof(float);
+    if (plane > 0) s = (int)std::min<int64_t>(s, ws_bytes / plane);
+    return s >= 2 ? s : 1;
+}
+
+size_t conv_workspace_bytes(int64_t M, int N, int Cin, int n_cu)
+{
+    const int s = conv_splits(M, N, Cin, n_cu, INT64_MAX);
+    return s > 1 ? (size_t)s * M * N * sizeof(float) : 0;
 }
 
 hipError_t launch_vae_conv(const ConvArgs &a, hipStream_t stream)
 {
     const int64_t M = (int64_t)a.n_tiles * a.T * a.Hr * a.Wr;
     if (M == 0) return hipSuccess;
-    return conv_tile_rows(M, a.Cout, cu_count_here()) == 128 ? launch_conv_bm<128>(a, stream)
-                                                             : launch_conv_bm<256>(a, stream);
+    const int splits = a.ws != nullptr ? conv_splits(M, a.Cout, a.Cin, cu_count_here(), a.ws_bytes) : 1;
+    return launch_conv(a, splits, stream);
 }
 
 hipError_t launch_vae_blend(const BlendArgs &a, hipStream_t stream)

@@ -81,7 +81,7 @@ regenvc_status regenvc_vae_split(int32_t H, int32_t W, int32_t ty, int32_t tx, i
 regenvc_status regenvc_vae_conv3d_fwd(const void *in, int32_t in_is_plane, const void *w, const void *bias,
                                       int32_t silu, void *out, int32_t T, int32_t H, int32_t W, int32_t Cin,
                                       int32_t Cout, const regenvc_vae_tile *tiles, int32_t n_tiles, int32_t Hr,
-                                      int32_t Wr, void *stream)
+                                      int32_t Wr, void *workspace, int64_t workspace_bytes, void *stream)
 {
     const char *fn = "regenvc_vae_conv3d_fwd";
     if (T < 1 || H < 1 || W < 1 || Hr < 1 || Wr < 1)
@@ -101,13 +101,38 @@ regenvc_status regenvc_vae_conv3d_fwd(const void *in, int32_t in_is_plane, const
     if (overlaps(ro, range_of(in, in_bytes)) || overlaps(ro, range_of(w, (int64_t)Cout * 27 * Cin * 2)) ||
         overlaps(ro, range_of(bias, (int64_t)Cout * 2)))
         return failf(REGENVC_ERR_INVALID_ARG, "%s: out overlaps an input", fn);
+    if (workspace != nullptr) {
+        if (workspace_bytes < 0) return failf(REGENVC_ERR_INVALID_ARG, "%s: workspace_bytes < 0", fn);
+        if (!aligned(workspace, 256))
+            return failf(REGENVC_ERR_UNSUPPORTED, "%s: workspace must be 256-byte aligned", fn);
+        const auto rw = range_of(workspace, workspace_bytes);
+        if (overlaps(rw, ro) || overlaps(rw, range_of(in, in_bytes)) ||
+            overlaps(rw, range_of(w, (int64_t)Cout * 27 * Cin * 2)) || overlaps(rw, range_of(bias, (int64_t)Cout * 2)))
+            return failf(REGENVC_ERR_INVALID_ARG, "%s: workspace overlaps another argument", fn);
+    }
     if ((st = regenvc::abi::device_ok()) != REGENVC_OK) return st;
     regenvc::ConvArgs a{};
     a.in = in, a.w = w, a.bias = bias, a.out = out;
     a.T = T, a.H = H, a.W = W, a.Cin = Cin, a.Cout = Cout, a.Hr = Hr, a.Wr = Wr, a.n_tiles = n_tiles;
     a.in_is_plane = in_is_plane != 0, a.silu = silu != 0;
+    a.ws = workspace, a.ws_bytes = workspace != nullptr ? workspace_bytes : 0;
     copy_tiles(a.tiles, tiles, n_tiles);
     return regenvc::abi::launch_status(regenvc::launch_vae_conv(a, static_cast<hipStream_t>(stream)), fn);
+}
+
+regenvc_status regenvc_vae_conv3d_workspace(int32_t T, int32_t Hr, int32_t Wr, int32_t n_tiles, int32_t Cin,
+                                            int32_t Cout, int32_t n_cu, int64_t *bytes)
+{
+    const char *fn = "regenvc_vae_conv3d_workspace";
+    if (bytes == nullptr) return failf(REGENVC_ERR_INVALID_ARG, "%s: bytes is NULL", fn);
+    if (T < 1 || Hr < 1 || Wr < 1 || n_tiles < 1 || n_tiles > REGENVC_VAE_MAX_TILES || n_cu < 1)
+        return failf(REGENVC_ERR_INVALID_ARG, "%s: bad sizes (T=%d Hr=%d Wr=%d n_tiles=%d n_cu=%d)", fn, T, Hr, Wr,
+                     n_tiles, n_cu);
+    if (Cin < 64 || Cout < 64 || Cin % 64 || Cout % 64)
+        return failf(REGENVC_ERR_UNSUPPORTED, "%s: channels Cin=%d Cout=%d must be multiples of 64", fn, Cin, Cout);
+    *bytes = (int64_t)regenvc::conv_workspace_bytes((int64_t)n_tiles * T * Hr * Wr, Cout, Cin, n_cu);
+    regenvc::abi::clear_error();
+    return REGENVC_OK;
 }
 
 regenvc_status regenvc_vae_blend(const void *tiles_out, const regenvc_vae_tile *tiles, int32_t n_tiles, int32_t Hr,

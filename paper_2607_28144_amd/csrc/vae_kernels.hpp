@@ -1,6 +1,7 @@
 // Internal launch interface of the spatially split VAE tile kernels.
 #pragma once
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 namespace regenvc {
@@ -28,8 +29,13 @@ struct ConvArgs {
     int32_t T, H, W, Cin, Cout, Hr, Wr, n_tiles;
     int32_t in_is_plane, silu;
     VaeTile tiles[kVaeMaxTiles];
+    void *ws;          // split-K partials (f32), or null: no split
+    int64_t ws_bytes;
 };
-int conv_tile_rows(int64_t M, int N, int n_cu);
+// K ranges a launch of M output rows uses with ws_bytes of workspace (1: none).
+int conv_splits(int64_t M, int N, int Cin, int n_cu, int64_t ws_bytes);
+// Workspace bytes that give a launch its full split (0: it does not split).
+size_t conv_workspace_bytes(int64_t M, int N, int Cin, int n_cu);
 hipError_t launch_vae_conv(const ConvArgs &a, hipStream_t stream);
 
 // Blended gather of the tiles' outputs [n][T][Hr][Wr][C] into the plane

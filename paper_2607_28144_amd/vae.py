@@ -35,12 +35,30 @@ def _check(t: torch.Tensor, name: str):
         raise ValueError(f"{name} must be a contiguous bf16 device tensor")
 
 
+_N_CU = {}
+
+
+def conv3d_workspace_bytes(T: int, Hr: int, Wr: int, n_tiles: int, Cin: int, Cout: int, device) -> int:
+    """Workspace bytes of the split-K form of one convolution on this device
+    (regenvc_vae_conv3d_workspace; host-only, 0 when it does not split)."""
+    idx = torch.device(device).index
+    idx = torch.cuda.current_device() if idx is None else idx
+    if idx not in _N_CU:
+        _N_CU[idx] = torch.cuda.get_device_properties(idx).multi_processor_count
+    out = ctypes.c_int64()
+    st = _lib.load().regenvc_vae_conv3d_workspace(T, Hr, Wr, n_tiles, Cin, Cout, _N_CU[idx], ctypes.byref(out))
+    _lib.check(st, "regenvc_vae_conv3d_workspace")
+    return out.value
+
+
 def conv3d(x: torch.Tensor, w: torch.Tensor, b: torch.Tensor, tiles, Hr: int, Wr: int, plane_hw=None,
-           silu: bool = False) -> torch.Tensor:
+           silu: bool = False, split_k: bool = True) -> torch.Tensor:
     """One causal 3D convolution over the listed tiles' regions
     (regenvc_vae_conv3d_fwd).  x: the plane [T, H, W, Cin] (plane_hw None),
     or the tiles' buffers [n, T, Hr, Wr, Cin] (plane_hw = (H, W), the plane's
-    size).  Returns [n, T, Hr, Wr, Cout]."""
+    size).  Returns [n, T, Hr, Wr, Cout].  split_k: hand the library the
+    workspace of its split-K form (a torch allocation), used when the tiles
+    alone would leave the GPU mostly idle."""
     for name, t in (("x", x), ("w", w), ("b", b)):
         _check(t, name)
     n = len(tiles)
@@ -58,8 +76,11 @@ def conv3d(x: torch.Tensor, w: torch.Tensor, b: torch.Tensor, tiles, Hr: int, Wr
         raise ValueError("w must be [Cout, 3, 3, 3, Cin] and b [Cout]")
     out = torch.empty((n, T, Hr, Wr, Cout), dtype=torch.bfloat16, device=x.device)
     arr = (_lib.VaeTile * n)(*tiles)
+    need = conv3d_workspace_bytes(T, Hr, Wr, n, Cin, Cout, x.device) if split_k else 0
+    ws = torch.empty(need, dtype=torch.uint8, device=x.device) if need > 0 else None
     st = _lib.load().regenvc_vae_conv3d_fwd(x.data_ptr(), is_plane, w.data_ptr(), b.data_ptr(), int(silu),
-                                            out.data_ptr(), T, H, W, Cin, Cout, arr, n, Hr, Wr, _stream(x.device))
+                                            out.data_ptr(), T, H, W, Cin, Cout, arr, n, Hr, Wr,
+                                            ws.data_ptr() if ws is not None else None, need, _stream(x.device))
     _lib.check(st, "regenvc_vae_conv3d_fwd")
     return out
 

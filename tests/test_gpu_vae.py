@@ -10,6 +10,8 @@ stack on the whole plane -- equal in exact arithmetic when the halo covers
 band + layers -- within two bf16 steps of each value plus 2^-8 of the RMS,
 room for the rare rounding flips that carry from one layer into the next.
 """
+import ctypes
+
 import numpy as np
 import pytest
 
@@ -115,16 +117,60 @@ def test_window_latent_tile_of_an_eight_way_split():
     60 x 104, 384 channels, split 2 x 4 (one tile per GPU of the node), halo
     4, band 2.  Tiles 1 (top row, inner column) and 4 (bottom-left) are
     checked stage by stage; one tile launched alone (one GPU's share) gives
-    bitwise the batched launch's values; the blend is checked everywhere."""
+    bitwise the batched launch's values when K is not split, and passes the
+    same per-element bounds in its split-K form (the single tile's 64 row
+    tiles run as 4 K ranges each); the blend is checked everywhere."""
     T, H, W, C = 7, 60, 104, 384
     X, convs, dx, dconvs, tl, Hr, Wr, y1, y2, out = stagewise("window", T, H, W, C, 2, 4, 4, 2, (1, 4), 72)
-    one1 = kern().conv3d(dx, *dconvs[0], [tl[1]], Hr, Wr, silu=True)
-    one2 = kern().conv3d(one1, *dconvs[1], [tl[1]], Hr, Wr, plane_hw=(H, W))
+    assert kern().conv3d_workspace_bytes(T, Hr, Wr, 1, C, C, dx.device) > 0  # the single tile splits K
+    assert kern().conv3d_workspace_bytes(T, Hr, Wr, 8, C, C, dx.device) == 0  # the batch does not
+    one1 = kern().conv3d(dx, *dconvs[0], [tl[1]], Hr, Wr, silu=True, split_k=False)
+    one2 = kern().conv3d(one1, *dconvs[1], [tl[1]], Hr, Wr, plane_hw=(H, W), split_k=False)
+    sk1 = kern().conv3d(dx, *dconvs[0], [tl[1]], Hr, Wr, silu=True)
+    sk2 = kern().conv3d(sk1, *dconvs[1], [tl[1]], Hr, Wr, plane_hw=(H, W))
     torch.cuda.synchronize()
     (r0, r1), (c0, c1) = region(tl[1])
     h, w = r1 - r0, c1 - c0
     assert torch.equal(one1[0, :, :h, :w], y1[1, :, :h, :w])
     assert torch.equal(one2[0, :, :h, :w], y2[1, :, :h, :w])
+    g1 = host(sk1)[0, :, :h, :w]
+    ref, tol = conv_ref(X[:, r0:r1, c0:c1], *convs[0], True)
+    check_bound("window tile 1 split-K conv 1 (SiLU)", g1, ref, tol)
+    ref, tol = conv_ref(g1, *convs[1], False)
+    check_bound("window tile 1 split-K conv 2", host(sk2)[0, :, :h, :w], ref, tol)
+
+
+def test_split_k_every_range_count():
+    """Small convolutions in the split-K form with workspaces that allow 2,
+    3 and 8 K ranges (and none): each against the oracle's per-element
+    bound, on a 1 x 2 split (two tiles, 64 channels in, 128 out)."""
+    T, H, W, Cin, Cout = 3, 9, 14, 64, 128
+    rng = np.random.default_rng(74)
+    x = synth.normal_bf16(rng, (T, H, W, Cin))
+    wb = synth.normal_bf16(rng, (Cout, 3, 3, 3, Cin), float(1.0 / np.sqrt(27 * Cin)))
+    bb = synth.normal_bf16(rng, (Cout,), 0.02)
+    X = widen(x)
+    tiles, Hr, Wr = kern().split(H, W, 1, 2, 3)
+    tl = list(tiles)
+    M = len(tl) * T * Hr * Wr
+    dx, dw, db = dev_bits(x), dev_bits(wb), dev_bits(bb)
+    from paper_2607_28144_amd import _lib
+    lib = _lib.load()
+    arr = (_lib.VaeTile * len(tl))(*tl)
+    for ranges in (0, 2, 3, 8):
+        out = torch.empty((len(tl), T, Hr, Wr, Cout), dtype=torch.bfloat16, device=dx.device)
+        nbytes = ranges * M * Cout * 4
+        ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dx.device) if ranges else None
+        st = lib.regenvc_vae_conv3d_fwd(dx.data_ptr(), 1, dw.data_ptr(), db.data_ptr(), 1, out.data_ptr(), T, H, W,
+                                        Cin, Cout, arr, len(tl), Hr, Wr, ws.data_ptr() if ws is not None else None,
+                                        nbytes, ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        _lib.check(st, "regenvc_vae_conv3d_fwd")
+        torch.cuda.synchronize()
+        g = host(out)
+        for i in range(len(tl)):
+            (r0, r1), (c0, c1) = region(tl[i])
+            ref, tol = conv_ref(X[:, r0:r1, c0:c1], wb, bb, True)
+            check_bound(f"split-K {ranges} ranges, tile {i}", g[i, :, :r1 - r0, :c1 - c0], ref, tol)
 
 
 def test_plain_crop_and_single_tile():
