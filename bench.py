@@ -417,8 +417,10 @@ def vae_leg(torch, dev, reps, warmup):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=20, help="untimed steps (the clock settles under load)")
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=100,
+                    help="untimed steps: the shader clock takes ~60 window self-attention calls (~40 ms) under "
+                         "load to settle, and calls within that time run up to 30 %% slower")
     ap.add_argument("--only", choices=["self", "cross", "share", "ring", "dual", "cross2", "copy", "normrope",
                                        "block", "vae"],
                     default=None,

@@ -29,8 +29,8 @@
  *   - Scratch memory: when the query tiles of an attention call do not fill
  *     whole rounds of the GPU's compute units, the leftover tiles are split
  *     along the keys and their partial results combined by a second kernel.
- *     Those partials live in a workspace of (split units) x 256 x (D + 1)
- *     floats (15.3 MB for 12 heads x 10920 tokens at D = 128; the exact size
+ *     Those partials live in a workspace of (split units) x (tile rows) x
+ *     (D + 1) floats (15.3 MB for 12 heads x 10920 tokens at D = 128; the exact size
  *     of a call is workspace_bytes of regenvc_attn_plan_query or
  *     regenvc_cross_attn_dual_plan_query).  A caller that binds a workspace
  *     with regenvc_attn_set_workspace supplies it and the library allocates
@@ -301,23 +301,27 @@ regenvc_status regenvc_qk_norm_rope(const regenvc_tensor *q_in, const regenvc_te
 /* Work plan of one attention call (regenvc_attn_fwd, regenvc_attn_partial_fwd
    or regenvc_cross_attn_fwd) of the given shape on a device with n_cu
    compute units (the calls themselves use the current device's count, 256
-   on MI355X).  Queries are processed in tiles of 256 of one (batch, head)
-   and keys in tiles of 64.  whole_tiles query tiles run as one workgroup
-   each; each of the split_tiles leftover tiles runs as key_ranges
-   workgroups over contiguous key ranges whose partials a second kernel
-   combines, and those partials occupy workspace_bytes of scratch memory
-   (0 when nothing is split; see "Scratch memory" above).
+   on MI355X).  Queries are processed in tiles of tile_rows of one (batch,
+   head) and keys in tiles of 64: tile_rows is 256, or 128 for calls with
+   fewer than 32 key tiles, which run two 128-row workgroups per compute
+   unit (so that one's query load and output stores overlap the other's
+   key loop).  whole_tiles query tiles run as one workgroup each; each of
+   the split_tiles leftover tiles runs as key_ranges workgroups over
+   contiguous key ranges whose partials a second kernel combines, and those
+   partials occupy workspace_bytes of scratch memory (0 when nothing is
+   split; see "Scratch memory" above).
      B, H, Sq >= 0; Skv >= 1; D in {64, 128}; n_cu >= 1; plan non-NULL.
    Host-only: makes no HIP call.  Returns REGENVC_ERR_INVALID_ARG or
    REGENVC_ERR_UNSUPPORTED (D, or more than 2^31 - 1 query tiles) on bad
    arguments, leaving *plan untouched. */
 typedef struct {
-    int32_t query_tiles; /* B * H * ceil(Sq / 256) */
+    int32_t query_tiles; /* B * H * ceil(Sq / tile_rows) */
     int32_t key_tiles;   /* ceil(Skv / 64) */
     int32_t whole_tiles;
     int32_t split_tiles;
     int32_t key_ranges;  /* per split tile; 0 when split_tiles == 0 */
     int64_t workspace_bytes;
+    int32_t tile_rows;   /* query rows per tile: 256 or 128 */
 } regenvc_attn_plan;
 
 regenvc_status regenvc_attn_plan_query(int32_t B, int32_t H, int32_t Sq, int32_t Skv, int32_t D,

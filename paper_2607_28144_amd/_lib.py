@@ -3,6 +3,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import threading
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libregenvc_attn.so")
 
@@ -21,7 +22,8 @@ class AttnPlan(ctypes.Structure):
     """regenvc_attn_plan: the work decomposition of one attention call."""
     _fields_ = [("query_tiles", ctypes.c_int32), ("key_tiles", ctypes.c_int32),
                 ("whole_tiles", ctypes.c_int32), ("split_tiles", ctypes.c_int32),
-                ("key_ranges", ctypes.c_int32), ("workspace_bytes", ctypes.c_int64)]
+                ("key_ranges", ctypes.c_int32), ("workspace_bytes", ctypes.c_int64),
+                ("tile_rows", ctypes.c_int32)]
 
 
 class VaeTile(ctypes.Structure):
@@ -124,7 +126,18 @@ def load(path: str | None = None) -> ctypes.CDLL:
     return lib
 
 
+_kept = threading.local()
+
+
+def keep_error_detail() -> None:
+    """Saves the library's error text of the failed call just made on this
+    thread, for the next check() (a later successful call clears the text)."""
+    _kept.detail = load().regenvc_last_error().decode(errors="replace")
+
+
 def check(status: int, fn: str) -> None:
+    kept = getattr(_kept, "detail", None)
+    _kept.detail = None
     if status != OK:
-        detail = load().regenvc_last_error().decode(errors="replace")
+        detail = kept if kept is not None else load().regenvc_last_error().decode(errors="replace")
         raise RegenvcError(status, fn, detail)

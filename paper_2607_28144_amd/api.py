@@ -12,6 +12,7 @@ from __future__ import annotations
 
 import ctypes
 import math
+import os
 from typing import List, Optional, Sequence, Tuple
 
 import torch
@@ -61,7 +62,8 @@ def _workspace_need(device: torch.device, B, H, Sq, Skv, D, Skv2: int = 0) -> in
     """Scratch bytes of one attention call (the library's host-only plan query
     with this device's compute-unit count)."""
     idx = device.index if device.index is not None else torch.cuda.current_device()
-    key = (idx, B, H, Sq, Skv, Skv2, D)
+    # the library picks its kernel, and with it the plan, by this variable too
+    key = (idx, B, H, Sq, Skv, Skv2, D, os.environ.get("REGENVC_ATTN_SCHEDULE"))
     need = _NEED.get(key)
     if need is None:
         if idx not in _N_CU:
@@ -95,7 +97,10 @@ def _with_workspace(device: torch.device, need: int, call):
             buf = _TOKEN[idx] = torch.empty(256, dtype=torch.uint8, device=device)
     _lib.check(lib.regenvc_attn_set_workspace(buf.data_ptr(), need), "regenvc_attn_set_workspace")
     try:
-        return call()
+        st = call()
+        if st != _lib.OK:  # keep the detail: the unbinding below clears it
+            _lib.keep_error_detail()
+        return st
     finally:
         lib.regenvc_attn_set_workspace(None, 0)
 
@@ -152,7 +157,7 @@ def attn_partial_fwd(q: torch.Tensor, k_chunk: torch.Tensor, v_chunk: torch.Tens
 def _chunk_plan(device: torch.device, B, H, Sq, bounds, D) -> int:
     """Scratch bytes of one chunked-partials call (host-only plan query)."""
     idx = device.index if device.index is not None else torch.cuda.current_device()
-    key = (idx, B, H, Sq, tuple(bounds), D)
+    key = (idx, B, H, Sq, tuple(bounds), D, os.environ.get("REGENVC_ATTN_SCHEDULE"))
     need = _NEED.get(key)
     if need is None:
         if idx not in _N_CU:

@@ -647,6 +647,7 @@ regenvc_status plan_query(const char *fn, int32_t B, int32_t H, int32_t Sq, int3
     plan->split_tiles = pl.n_tiles - pl.n_dp;
     plan->key_ranges = pl.n_units > 0 ? pl.seg + pl.seg2 : 0;
     plan->workspace_bytes = (int64_t)regenvc::workspace_bytes(pl, D);
+    plan->tile_rows = pl.bm;
     g_last_error[0] = '\0';
     return REGENVC_OK;
 }
@@ -695,6 +696,7 @@ regenvc_status regenvc_attn_partials_plan_query(int32_t B, int32_t H, int32_t Sq
     plan->split_tiles = pl.n_tiles - pl.n_dp;
     plan->key_ranges = pl.n_units > 0 ? pl.seg : 0;
     plan->workspace_bytes = (int64_t)regenvc::workspace_bytes(pl, D);
+    plan->tile_rows = pl.bm;
     g_last_error[0] = '\0';
     return REGENVC_OK;
 }

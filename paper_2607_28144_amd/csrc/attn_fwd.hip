@@ -101,7 +101,7 @@ constexpr float kSpecLimit = 256.f;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-template <int D, int STAGES = kStages>
+template <int D, int STAGES = kStages, int THREADS = kThreads>
 struct Geo {
     static constexpr int NCH = D / 8;                      // 16-byte chunks per row
     static constexpr int DS = D / 16;                      // k-steps of Q K^T
@@ -109,8 +109,8 @@ struct Geo {
     static constexpr int TILE = kBlockN * D * 2;           // bytes of one K or V tile
     static constexpr int STAGE = 2 * TILE;                 // K tile then V tile
     static constexpr int LDS = STAGES * STAGE;
-    static constexpr int LOADS = kBlockN * NCH / kThreads; // 16-byte loads per thread per tensor per tile
-    static_assert(LOADS >= 1 && (kBlockN * NCH) % kThreads == 0, "tile load split");
+    static constexpr int LOADS = kBlockN * NCH / THREADS;  // 16-byte loads per thread per tensor per tile
+    static_assert(LOADS >= 1 && (kBlockN * NCH) % THREADS == 0, "tile load split");
 };
 
 // LDS placement of 16-byte chunk `ch` of tile row `row` (an involution in ch).
@@ -432,11 +432,10 @@ __device__ __forceinline__ float load_run(const AttnArgs &a, int b, int h, int q
 // ones; a split tile's key range writes its normalized partial to the
 // workspace instead.  lsum and rsum are this lane's halves of l and l_r (the
 // other halves are in lane^32).
-template <int D, bool OUT_F32, bool ACC>
+template <int D, bool OUT_F32, bool ACC, int BM>
 __device__ __forceinline__ void store_row(const AttnArgs &a, const AttnPlan &pl, const f32x16 (&oacc)[D / 32],
                                           float lsum, float rsum, float mref, int b, int h, int qi, int qrow, int slot)
 {
-    constexpr int BM = kWaves * 32;
     constexpr int DB = D / 32;
     const int hi = (threadIdx.x >> 5) & 1;
     const float lt = pair_sum(lsum);
@@ -614,17 +613,24 @@ __device__ __forceinline__ void wait_vmcnt()
 // allocation).  A dual launch runs the key pipeline twice over one set of Q
 // fragments: first context, then, with the first result parked in LDS as
 // bf16 (the precision of a single context-attention output), the second.
-template <int D, bool OUT_F32, bool ACC, bool DUAL = false>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+template <int D, bool OUT_F32, bool ACC, bool DUAL = false, int WAVES = kWaves>
+__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_kernel(AttnArgs a_in, AttnPlan pl)
 {
-    using G = Geo<D>;
+    // Paired launches (WAVES = 4): two workgroups of 128 query rows share a
+    // CU, one wave of each per SIMD, so that one's Q load and output drain
+    // run beside the other's key loop; K and V then go through rings of two
+    // tiles each (64 KB of LDS per workgroup for d = 128), see `step`.
+    constexpr bool PAIRED = WAVES != kWaves;
+    static_assert(!PAIRED || (WAVES == 4 && !DUAL), "paired launches: 4 waves, one context");
+    constexpr int THREADS = 64 * WAVES;
+    using G = Geo<D, PAIRED ? 2 : kStages, THREADS>;
     constexpr int NCH = G::NCH, DS = G::DS, DB = G::DB, LOADS = G::LOADS;
-    constexpr int BM = kWaves * 32;
+    constexpr int BM = WAVES * 32;
     constexpr int PER_TILE = 2 * LOADS;  // copies in flight per thread per tile (K and V)
 
     // dual launches: + the first context's normalized O (bf16), 16-byte chunk
-    // j of thread t at byte G::LDS + 16 * (j * kThreads + t)
+    // j of thread t at byte G::LDS + 16 * (j * THREADS + t)
     __shared__ __attribute__((aligned(1024))) char smem[G::LDS + (DUAL ? BM * D * 2 : 0)];
 
     const int lane = threadIdx.x & 63;
@@ -736,8 +742,33 @@ void attn_fwd_kernel(AttnArgs a_in, AttnPlan pl)
             vb_copy += v_step;
         }
     };
-    auto next_stage = [](int st) { return st == kStages - 1 ? 0 : st + 1; };
-    static_assert(kAhead == 2 && kStages == 3, "the step issues tile t+2 into the stage of tile t-1");
+    auto next_stage = [](int st) { return st == G::LDS / G::STAGE - 1 ? 0 : st + 1; };
+    static_assert(PAIRED || (kAhead == 2 && kStages == 3), "the step issues tile t+2 into the stage of tile t-1");
+    // Paired launches: one tensor's copy of tile tl into the K or V half of
+    // the stage at LDS byte dst (same lane layout and clamping as above).
+    auto issue_one = [&](int tl, uint32_t dst, auto is_v) __attribute__((always_inline)) {
+        constexpr bool V = decltype(is_v)::value;
+        const uint16_t *base = V ? vp : kp;
+        const int64_t ss = V ? src.v_ss : src.k_ss;
+        if (src.off32 && tl <= last_full) {
+            const uint16_t *tb = base + (int64_t)tl * kBlockN * ss;
+#pragma unroll
+            for (int j = 0; j < LOADS; ++j)
+                lds_dma16_s(tb, V ? vofs[j] : kofs[j], dst + (wave * LOADS + j) * 1024);
+        } else {
+            const int key0 = tl * kBlockN;
+            const int last = Skv - 1 - key0;
+#pragma unroll
+            for (int j = 0; j < LOADS; ++j) {
+                const int blk = wave * LOADS + j;
+                const int slot16 = blk * 64 + lane;
+                const int row = slot16 / NCH, phys = slot16 % NCH;
+                const int64_t key = key0 + min(row, last);
+                const int ch = V ? v_slot<NCH>(row, phys) : k_slot<NCH>(row, phys);
+                lds_dma16(base + key * ss + ch * 8, dst + blk * 1024);
+            }
+        }
+    };
 
     // Per-lane LDS byte offsets of the MFMA operand fragments (stage 0).
     int koff[DS];
@@ -936,17 +967,29 @@ void attn_fwd_kernel(AttnArgs a_in, AttnPlan pl)
         nm = -mref;
     };
 
-    // Prologue: kAhead tiles in flight; S of the first tile.
-    int st = kt0 % kStages;  // stage of tile t
-    {
+    // Prologue: kAhead tiles in flight (paired launches: K of the first two
+    // tiles and V of the first); S of the first tile.
+    int st = kt0 % (G::LDS / G::STAGE);  // stage of tile t
+    if constexpr (PAIRED) {
+        const uint32_t s0 = lds0 + st * G::STAGE;
+        issue_one(kt0, s0, std::false_type{});
+        if (kt1 - kt0 > 1) {
+            issue_one(kt0 + 1, lds0 + (st ^ 1) * G::STAGE, std::false_type{});
+            issue_one(kt0, s0 + G::TILE, std::true_type{});
+            wait_vmcnt<2 * LOADS>();
+        } else {
+            issue_one(kt0, s0 + G::TILE, std::true_type{});
+            wait_vmcnt<LOADS>();
+        }
+    } else {
         int sl = st;
 #pragma unroll
         for (int i = 0; i < kAhead; ++i) {
             issue_next(sl);
             sl = next_stage(sl);
         }
+        wait_vmcnt<(kAhead - 1) * PER_TILE>();
     }
-    wait_vmcnt<(kAhead - 1) * PER_TILE>();
     __syncthreads();
     qk(st, scur);
 
@@ -958,7 +1001,20 @@ void attn_fwd_kernel(AttnArgs a_in, AttnPlan pl)
         constexpr bool MASK = decltype(mask)::value;
         const int st1 = next_stage(st);  // stage of tile t+1
         // ---- phase X
-        if constexpr (HAS_NEXT) {
+        if constexpr (PAIRED) {
+            // K of tile t+1 and V of tile t were copied during the previous
+            // step (or the prologue); K of tile t+2 goes into the stage whose
+            // K (tile t) the previous step's Q K^T consumed, V of tile t+1
+            // into the stage whose V (tile t-1) its P V consumed.
+            wait_vmcnt<0>();  // this wave's copies landed
+            __syncthreads();  // ... and every other wave's, which is past the previous step
+            if (t + 2 < kt1) issue_one(t + 2, lds0 + st * G::STAGE, std::false_type{});
+            if (t + 1 < kt1) issue_one(t + 1, lds0 + st1 * G::STAGE + G::TILE, std::true_type{});
+            if constexpr (HAS_NEXT)
+                qk_softmax(st1, sc, sn);
+            else
+                softmax_block<MASK>(sc, c, mref, lsum, rsum, p, alpha, upd, t * kBlockN, Skv);
+        } else if constexpr (HAS_NEXT) {
             // tiles up to t + kAhead - 1 have been issued; tile t+1 must have
             // landed, so at most kAhead - 2 tiles' copies may still be in flight
             wait_vmcnt<(kAhead - 2) * PER_TILE>();  // this wave's copies of tile t+1 landed
@@ -1013,14 +1069,14 @@ void attn_fwd_kernel(AttnArgs a_in, AttnPlan pl)
             bf16x8 w;
 #pragma unroll
             for (int e = 0; e < 8; ++e) w[e] = (__bf16)(oacc[j / 2][(j % 2) * 8 + e] * inv);
-            *(lds_bf16x8 *)(park + j * kThreads * 16) = w;
+            *(lds_bf16x8 *)(park + j * THREADS * 16) = w;
         }
         __syncthreads();  // every wave is done with the ring before the second pass refills it
     }
     }
 
     if (slot >= 0 || OUT_F32 || ACC) {
-        store_row<D, OUT_F32, ACC>(a, pl, oacc, lsum, rsum, mref, b, h, qi, qrow, slot);
+        store_row<D, OUT_F32, ACC, BM>(a, pl, oacc, lsum, rsum, mref, b, h, qi, qrow, slot);
         return;
     }
     // whole tile, bf16 output: final values in oacc, then full-row stores
@@ -1040,7 +1096,7 @@ void attn_fwd_kernel(AttnArgs a_in, AttnPlan pl)
         char *orow = static_cast<char *>(a.o) + ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * 2;
 #pragma unroll
         for (int j = 0; j < DB * 2; ++j) {
-            const bf16x8 o1 = *(const lds_bf16x8 *)(park + j * kThreads * 16);
+            const bf16x8 o1 = *(const lds_bf16x8 *)(park + j * THREADS * 16);
 #pragma unroll
             for (int half = 0; half < 2; ++half) {
                 const int db = j / 2, gq = (j % 2) * 2 + half;
@@ -1541,17 +1597,27 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
 // The partials are visited in batches of FB whose LSE and O loads are all
 // issued before any of them is used, combined online (running max, sum and
 // weighted O), so the loop is not a chain of dependent memory accesses.
+// Key-range slices of the fixup: the waves of a workgroup take the same 64
+// (row, 4-dim) pairs, wave i merging key ranges i, i + kFixSlices, ...; the
+// first wave combines the slices' results (read through LDS) and stores.
+// Each lane then waits for one batch of partial loads instead of several in
+// turn, and the grid has kFixSlices times as many workgroups.
+constexpr int kFixSlices = 4;
+
 template <bool OUT_F32>
-__global__ __launch_bounds__(256) void split_fixup_kernel(AttnArgs a_in, AttnPlan pl)
+__global__ __launch_bounds__(64 * kFixSlices) void split_fixup_kernel(AttnArgs a_in, AttnPlan pl)
 {
-    constexpr int BM = kWaves * 32;
+    const int BM = pl.bm;
     constexpr int FB = 8;
+    __shared__ float red[2][kFixSlices - 1][6][64];
     const int per_row = a_in.D / 4;
-    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int slice = threadIdx.x >> 6;
     const int64_t rows = (int64_t)(pl.n_tiles - pl.n_dp) * BM;
-    const int64_t row = gid / per_row;
-    if (row >= rows) return;
-    const int d = (int)(gid % per_row) * 4;
+    const int64_t pair = (int64_t)blockIdx.x * 64 + lane;
+    // lanes past the last row merge the last one again (in bounds) and store nothing
+    const int64_t row = min(pair / per_row, rows - 1);
+    const int d = (int)(pair % per_row) * 4;
     const int j = (int)(row / BM), r = (int)(row % BM);
     int tile = pl.n_dp + j;
     const AttnArgs a = chunk_of(a_in, pl, tile);
@@ -1559,26 +1625,28 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(AttnArgs a_in, AttnPla
     const int bh = tile / pl.n_qtiles;
     const int h = bh % a.H, b = bh / a.H;
     const int qi = qt * BM + r;
-    if (qi >= a.Sq) return;
-    // LSE merge of n units from u0 on: (max m, sum s, weighted O acc)
+    const bool live = pair / per_row < rows && qi < a.Sq;
+    // LSE merge of this slice's units among n from u0 on: (max m, sum s,
+    // weighted O acc); m = -inf, s = 0 and acc = 0 for a slice without units
     auto merge_units = [&](int64_t u0, int n, float &m, float &s, f32x4 &acc) {
         m = -INFINITY;
         s = 0.f;
         acc = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int c0 = 0; c0 < n; c0 += FB) {
+        for (int c0 = slice; c0 < n; c0 += FB * kFixSlices) {
             float l[FB];
             f32x4 o[FB];
 #pragma unroll
             for (int k = 0; k < FB; ++k) {
-                const int64_t u = u0 + min(c0 + k, n - 1);
-                l[k] = c0 + k < n ? pl.ws_lse[u * BM + r] : -INFINITY;
+                const int c = c0 + k * kFixSlices;
+                const int64_t u = u0 + min(c, n - 1);
+                l[k] = c < n ? pl.ws_lse[u * BM + r] : -INFINITY;
                 o[k] = *reinterpret_cast<const f32x4 *>(pl.ws_o + (u * BM + r) * a.D + d);
             }
             float mb = m;
 #pragma unroll
             for (int k = 0; k < FB; ++k) mb = fmaxf(mb, l[k]);
-            // every key range holds at least one key, so mb is finite from the
-            // first batch on
+            // every key range holds at least one key and each batch starts
+            // with a unit, so mb is finite
             const float sc = expf(m - mb);
             s *= sc;
             acc *= sc;
@@ -1591,18 +1659,55 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(AttnArgs a_in, AttnPla
             m = mb;
         }
     };
+    // The slices' results combined on the first wave (buffer i of red);
+    // slice 0 always holds unit 0, so the common maximum is finite.
+    auto combine = [&](int i, float &m, float &s, f32x4 &acc) {
+        if (slice > 0) {
+            float *e = &red[i][slice - 1][0][lane];
+            e[0] = m;
+            e[64] = s;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) e[(2 + k) * 64] = acc[k];
+        }
+        __syncthreads();
+        if (slice == 0) {
+            float ms[kFixSlices];
+            ms[0] = m;
+#pragma unroll
+            for (int t = 1; t < kFixSlices; ++t) ms[t] = red[i][t - 1][0][lane];
+            float mx = ms[0];
+#pragma unroll
+            for (int t = 1; t < kFixSlices; ++t) mx = fmaxf(mx, ms[t]);
+            const float w0 = expf(m - mx);
+            s *= w0;
+            acc *= w0;
+#pragma unroll
+            for (int t = 1; t < kFixSlices; ++t) {
+                const float w = expf(ms[t] - mx);
+                s += w * red[i][t - 1][1][lane];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) acc[k] += w * red[i][t - 1][2 + k][lane];
+            }
+            m = mx;
+        }
+    };
     const int64_t u0 = (int64_t)j * (pl.seg + pl.seg2);
     float m, s;
     f32x4 acc;
     merge_units(u0, pl.seg, m, s, acc);
+    combine(0, m, s, acc);
+    float m2 = 0.f, s2 = 1.f;
+    f32x4 acc2{};
+    if (pl.seg2 > 0) {  // dual context: the second context's units, merged alike
+        merge_units(u0 + pl.seg, pl.seg2, m2, s2, acc2);
+        combine(1, m2, s2, acc2);
+    }
+    if (slice != 0 || !live) return;
     const float L = m + logf(s);
     char *orow = static_cast<char *>(a.o) +
                  ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * (OUT_F32 ? 4 : 2);
     const int64_t li = ((int64_t)b * a.H + h) * a.Sq + qi;
-    if (pl.seg2 > 0) {  // dual context: the second context's units, merged alike; the two results summed
-        float m2, s2;
-        f32x4 acc2;
-        merge_units(u0 + pl.seg, pl.seg2, m2, s2, acc2);
+    if (pl.seg2 > 0) {  // the two contexts' results summed
         put_out4<OUT_F32>(orow, RunMerge{1.f, 1.0f / s, L, true}, d, acc, acc2 * (1.0f / s2));
         if (d == 0) {
             if (a.lse != nullptr) a.lse[li] = L;
@@ -1615,17 +1720,22 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(AttnArgs a_in, AttnPla
     if (a.run_lse != nullptr) w = run_merge(load_run(a, b, h, qi, d, 0, run), L);
     w.wc *= 1.0f / s;
     put_out4<OUT_F32>(orow, w, d, acc, run[0]);
-    if (a.lse != nullptr && d == 0) a.lse[((int64_t)b * a.H + h) * a.Sq + qi] = w.lse;
+    if (a.lse != nullptr && d == 0) a.lse[li] = w.lse;
 }
 
 // Chooses the work plan by a cost model in units of one key-tile iteration
 // of one workgroup: whole tiles cost n_kt + 1 (prologue and epilogue), a
 // split unit costs its key range + 1.5 (the partial store), and the partials'
 // write + read traffic is priced at 5 TB/s against ~1 us per iteration.
-AttnPlan make_plan(int n_qtiles, int n_tiles, int n_kt, int n_cu, int D)
+// n_cu counts workgroup slots: in paired launches (128-row tiles) two per
+// CU; there the tiles of a last, partial round that leaves each of them a
+// CU of its own run at about 0.65 of the paired time, and a split adds the
+// fixup launch (~2 iterations).
+AttnPlan make_plan(int n_qtiles, int n_tiles, int n_kt, int n_cu, int D, int BM)
 {
-    constexpr int BM = kWaves * 32;
+    const bool paired = BM != kWaves * 32;
     AttnPlan pl{};
+    pl.bm = BM;
     pl.n_qtiles = n_qtiles;
     pl.n_tiles = n_tiles;
     pl.n_kt = n_kt;
@@ -1633,9 +1743,10 @@ AttnPlan make_plan(int n_qtiles, int n_tiles, int n_kt, int n_cu, int D)
     pl.seg = 1;
     pl.n_units = 0;
     const double whole = n_kt + 1.0;
-    double best = (double)((n_tiles + n_cu - 1) / n_cu) * whole;
     const int rounds = n_tiles / n_cu;
     const int rem = n_tiles - rounds * n_cu;
+    const double tail = rem == 0 ? 0.0 : (paired && rem <= n_cu / 2 ? 0.65 : 1.0) * whole;
+    double best = rounds * whole + tail;
     if (rem == 0 || n_kt < 2) return pl;
     for (int seg = 2; seg <= n_kt && seg <= 256; ++seg) {
         const int64_t units = (int64_t)rem * seg;
@@ -1643,7 +1754,7 @@ AttnPlan make_plan(int n_qtiles, int n_tiles, int n_kt, int n_cu, int D)
         const int64_t sk_rounds = (units + n_cu - 1) / n_cu;
         const int len = (n_kt + seg - 1) / seg;
         const double traffic = 2.0 * units * BM * (D + 1) * 4 / 5e12 / 1e-6;
-        const double cost = rounds * whole + sk_rounds * (len + 1.5) + traffic;
+        const double cost = rounds * whole + sk_rounds * (len + 1.5) + traffic + (paired ? 2.0 : 0.0);
         if (cost < best) {
             best = cost;
             pl.n_dp = rounds * n_cu;
@@ -1662,6 +1773,7 @@ AttnPlan make_plan_dual(int n_qtiles, int n_tiles, int n_kt, int n_kt2, int n_cu
 {
     constexpr int BM = kWaves * 32;
     AttnPlan pl{};
+    pl.bm = BM;
     pl.n_qtiles = n_qtiles;
     pl.n_tiles = n_tiles;
     pl.n_kt = n_kt;
@@ -1741,9 +1853,23 @@ int forced_schedule()
 {
     const char *e = getenv("REGENVC_ATTN_SCHEDULE");
     if (e == nullptr) return 0;
-    if (strcmp(e, "pingpong") == 0) return 1;
-    if (strcmp(e, "interleaved") == 0) return 2;
+    if (strcmp(e, "pingpong") == 0) return kSchedPingPong;
+    if (strcmp(e, "interleaved") == 0) return kSchedInterleaved;
+    if (strcmp(e, "paired") == 0) return kSchedPaired;
     return 0;
+}
+
+// Kernel of a launch with n_kt key tiles per whole tile: the ping-pong
+// schedule from kPingPongMinTiles key tiles on, the paired interleaved one
+// below; dual-context launches always take the 8-wave interleaved kernel
+// (its parked first result needs the LDS), chunked ones never the paired.
+int pick_schedule(int n_kt, bool dual, bool chunked)
+{
+    if (dual) return kSchedInterleaved;
+    int s = forced_schedule();
+    if (s == 0) s = n_kt >= kPingPongMinTiles ? kSchedPingPong : kSchedPaired;
+    if (chunked && s == kSchedPaired) s = kSchedInterleaved;
+    return s;
 }
 
 // The work plan of launch `a` on n_cu compute units.
@@ -1756,7 +1882,6 @@ bool plan_for(const AttnArgs &a, int n_cu, AttnPlan *pl)
 template <int D, bool OUT_F32>
 hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream, const Workspace &given)
 {
-    constexpr int BM = kWaves * 32;
     AttnPlan pl{};
     if (OUT_F32 && a.k2 != nullptr) return hipErrorInvalidValue;  // dual context: bf16 output only
     if (a.n_chunks > 1 && (!OUT_F32 || a.k2 != nullptr || a.run_lse != nullptr)) return hipErrorInvalidValue;
@@ -1775,29 +1900,33 @@ hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream, const Workspace 
             buf = ws;
         }
         pl.ws_o = static_cast<float *>(buf);
-        pl.ws_lse = pl.ws_o + (size_t)pl.n_units * BM * D;
+        pl.ws_lse = pl.ws_o + (size_t)pl.n_units * pl.bm * D;
     }
-    const dim3 grid((unsigned)(pl.n_dp + pl.n_units)), block(kThreads);
-    const int forced = forced_schedule();
-    const bool pp = forced == 1 || (forced == 0 && pl.n_kt >= kPingPongMinTiles);
+    const dim3 grid((unsigned)(pl.n_dp + pl.n_units));
+    const dim3 block(pl.sched == kSchedPaired ? 256 : kThreads);
+    const bool pp = pl.sched == kSchedPingPong;
     if (a.k2 != nullptr) {
         if constexpr (!OUT_F32)
             hipLaunchKernelGGL((attn_fwd_kernel<D, false, false, true>), grid, block, 0, stream, a, pl);
     } else if (a.run_lse != nullptr) {
         if (pp)
             hipLaunchKernelGGL((attn_fwd_pingpong_kernel<D, OUT_F32, true>), grid, block, 0, stream, a, pl);
+        else if (pl.sched == kSchedPaired)
+            hipLaunchKernelGGL((attn_fwd_kernel<D, OUT_F32, true, false, 4>), grid, block, 0, stream, a, pl);
         else
             hipLaunchKernelGGL((attn_fwd_kernel<D, OUT_F32, true>), grid, block, 0, stream, a, pl);
     } else if (pp) {
         hipLaunchKernelGGL((attn_fwd_pingpong_kernel<D, OUT_F32, false>), grid, block, 0, stream, a, pl);
+    } else if (pl.sched == kSchedPaired) {
+        hipLaunchKernelGGL((attn_fwd_kernel<D, OUT_F32, false, false, 4>), grid, block, 0, stream, a, pl);
     } else {
         hipLaunchKernelGGL((attn_fwd_kernel<D, OUT_F32, false>), grid, block, 0, stream, a, pl);
     }
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && pl.n_units > 0) {
-        const int64_t threads = (int64_t)(pl.n_tiles - pl.n_dp) * BM * (D / 4);
-        hipLaunchKernelGGL(split_fixup_kernel<OUT_F32>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
-                           stream, a, pl);
+        const int64_t pairs = (int64_t)(pl.n_tiles - pl.n_dp) * pl.bm * (D / 4);
+        hipLaunchKernelGGL(split_fixup_kernel<OUT_F32>, dim3((unsigned)((pairs + 63) / 64)), dim3(64 * kFixSlices),
+                           0, stream, a, pl);
         e = hipGetLastError();
     }
     if (ws != nullptr) {
@@ -1811,8 +1940,11 @@ hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream, const Workspace 
 
 bool plan_attn(int B, int H, int Sq, int Skv, int D, int n_cu, AttnPlan *out, int Skv2)
 {
-    constexpr int BM = kWaves * 32;
     if (B < 0 || H < 0 || Sq < 0 || Skv < 1 || n_cu < 1) return false;
+    const int sched = pick_schedule((int)(((int64_t)Skv + kBlockN - 1) / kBlockN), Skv2 > 0, false);
+    // paired launches: 128-row tiles, two resident per CU
+    const int BM = sched == kSchedPaired ? 128 : kWaves * 32;
+    const int slots = sched == kSchedPaired && n_cu <= 0x3fffffff ? 2 * n_cu : n_cu;
     const int64_t n_qtiles = ((int64_t)Sq + BM - 1) / BM;  // < 2^24
     const int64_t per_batch = n_qtiles * H;                 // < 2^55: no overflow
     if (per_batch > 0x7fffffff || (B > 0 && per_batch > 0x7fffffff / B)) return false;
@@ -1823,7 +1955,8 @@ bool plan_attn(int B, int H, int Sq, int Skv, int D, int n_cu, AttnPlan *out, in
         *out = make_plan_dual((int)n_qtiles, (int)n_tiles, n_kt, (int)(((int64_t)Skv2 + kBlockN - 1) / kBlockN), n_cu,
                               D);
     else
-        *out = make_plan((int)n_qtiles, (int)n_tiles, n_kt, n_cu, D);
+        *out = make_plan((int)n_qtiles, (int)n_tiles, n_kt, slots, D, BM);
+    out->sched = sched;
     return true;
 }
 
@@ -1838,7 +1971,8 @@ bool plan_attn_chunks(int B, int H, int Sq, int n_chunks, const int32_t *clen, i
     if (n_qtiles * H > 0x7fffffff || per_chunk > 0x7fffffff / n_chunks) return false;
     auto kt = [](int len) { return (int)(((int64_t)len + kBlockN - 1) / kBlockN); };
     const int n_kt = kt(clen[n_chunks - 1]);
-    *out = make_plan((int)n_qtiles, (int)(per_chunk * n_chunks), n_kt, n_cu, D);
+    *out = make_plan((int)n_qtiles, (int)(per_chunk * n_chunks), n_kt, n_cu, D, BM);
+    out->sched = pick_schedule(n_kt, false, true);
     out->tiles_per_chunk = (int)per_chunk;
     if (out->n_units > 0 && per_chunk > 0) {
         // the split tiles are the last ones: their chunks must all have n_kt key tiles
@@ -1855,7 +1989,7 @@ bool plan_attn_chunks(int B, int H, int Sq, int n_chunks, const int32_t *clen, i
 
 size_t workspace_bytes(const AttnPlan &pl, int D)
 {
-    return (size_t)pl.n_units * (kWaves * 32) * (D + 1) * sizeof(float);
+    return (size_t)pl.n_units * pl.bm * (D + 1) * sizeof(float);
 }
 
 int device_cu_count()

@@ -8,6 +8,11 @@ namespace regenvc {
 
 constexpr int kMaxChunks = 16;  // key chunks of one chunked-partials launch
 
+// Attention kernels (AttnPlan::sched): the ping-pong schedule (8 waves, 256
+// query rows), the interleaved one (the same tile), and the interleaved one
+// in pairs (4 waves, 128 query rows, two workgroups resident per CU).
+constexpr int kSchedPingPong = 1, kSchedInterleaved = 2, kSchedPaired = 3;
+
 // One attention launch: Q [B,Sq,H,D], K/V [B,Skv,H,D] (bf16, element strides,
 // d contiguous); O [B,Sq,H,D] bf16 or f32; optional f32 LSE [B,H,Sq].
 struct AttnArgs {
@@ -69,6 +74,8 @@ struct AttnPlan {
     int32_t n_kt2;     // key tiles of the second context (dual launches; else 0)
     int32_t seg2;      // key ranges of a split tile over the second context (else 0)
     int32_t tiles_per_chunk;  // chunked partials: B * H * n_qtiles (else 0); n_kt is the last chunk's
+    int32_t bm;        // query rows per tile: 256, or 128 for the paired interleaved kernel
+    int32_t sched;     // kernel: kSchedPingPong, kSchedInterleaved or kSchedPaired
     float *ws_o;       // [n_units][query tile rows][D] partial O (normalized)
     float *ws_lse;     // [n_units][query tile rows] partial LSE
 };

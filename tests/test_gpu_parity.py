@@ -339,11 +339,12 @@ def test_empty_query_set_is_a_no_op():
     assert o.numel() == 0 and lse.numel() == 0
 
 
-# ------------------------------------------------------------------ both schedules
+# ------------------------------------------------------------------ every schedule
 # Launches with many key tiles run the ping-pong schedule, short ones the
-# interleaved one; REGENVC_ATTN_SCHEDULE forces either, so that each is
-# checked on every case below whatever its length.
-SCHEDULES = ["interleaved", "pingpong"]
+# interleaved kernel in pairs (two 128-row workgroups per CU); dual-context
+# launches the 8-wave interleaved one.  REGENVC_ATTN_SCHEDULE forces any of
+# the three, so that each is checked on every case below whatever its length.
+SCHEDULES = ["interleaved", "pingpong", "paired"]
 
 
 @pytest.fixture(params=SCHEDULES)

@@ -85,7 +85,7 @@ def test_ring_rank_share_config():
     assert d_o <= 2 ** -7 and d_l <= 1e-5
 
 
-@pytest.mark.parametrize("schedule", ["interleaved", "pingpong"])
+@pytest.mark.parametrize("schedule", ["interleaved", "pingpong", "paired"])
 @pytest.mark.parametrize("bounds", [[0, 1, 100, 101, 777], [0, 640, 777]])
 def test_ring_ragged_chunks_from_no_keys(schedule, bounds, monkeypatch):
     """Uneven and single-token chunks, 300 queries (a ragged query tile),

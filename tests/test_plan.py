@@ -8,7 +8,8 @@ import pytest
 from paper_2607_28144_amd import _lib
 from paper_2607_28144_amd.api import attn_plan
 
-BM, BN = 256, 64
+BN = 64
+PAIRED_BELOW = 32  # key tiles: shorter calls run two 128-row workgroups per CU
 
 
 def ceil_div(a, b):
@@ -16,14 +17,17 @@ def ceil_div(a, b):
 
 
 def check_invariants(p, B, H, Sq, Skv, D, n_cu):
-    assert p["query_tiles"] == B * H * ceil_div(Sq, BM)
+    BM = p["tile_rows"]
     assert p["key_tiles"] == ceil_div(Skv, BN)
+    assert BM == (128 if p["key_tiles"] < PAIRED_BELOW else 256)
+    slots = n_cu * (2 if BM == 128 else 1)  # workgroups resident at once
+    assert p["query_tiles"] == B * H * ceil_div(Sq, BM)
     assert p["whole_tiles"] + p["split_tiles"] == p["query_tiles"]
-    assert 0 <= p["split_tiles"] < n_cu
+    assert 0 <= p["split_tiles"] < slots
     if p["split_tiles"]:
-        # only the tiles of a last, partial round over the compute units are split
-        assert p["whole_tiles"] % n_cu == 0
-        assert p["whole_tiles"] == (p["query_tiles"] // n_cu) * n_cu
+        # only the tiles of a last, partial round over the workgroup slots are split
+        assert p["whole_tiles"] % slots == 0
+        assert p["whole_tiles"] == (p["query_tiles"] // slots) * slots
         assert 2 <= p["key_ranges"] <= p["key_tiles"]
     else:
         assert p["key_ranges"] == 0
@@ -37,7 +41,7 @@ def test_window_plan():
     p = attn_plan(1, 12, 10920, 10920, 128)
     check_invariants(p, 1, 12, 10920, 10920, 128, 256)
     assert p == {"query_tiles": 516, "key_tiles": 171, "whole_tiles": 512, "split_tiles": 4,
-                 "key_ranges": 29, "workspace_bytes": 15_323_136}
+                 "key_ranges": 29, "workspace_bytes": 15_323_136, "tile_rows": 256}
 
 
 def test_share_plan_splits_nothing():
@@ -49,10 +53,21 @@ def test_share_plan_splits_nothing():
 
 
 def test_cross_plan():
-    """Cross-attention to 512 context tokens: 8 key tiles, split one per range."""
+    """Cross-attention to 512 context tokens: 8 key tiles, so 128-row tiles
+    two per CU; the 1032 tiles are two rounds of 512 plus 8, which run whole
+    (each with a CU to itself) rather than split with a fixup launch."""
     p = attn_plan(1, 12, 10920, 512, 128)
     check_invariants(p, 1, 12, 10920, 512, 128, 256)
-    assert (p["key_tiles"], p["split_tiles"], p["key_ranges"]) == (8, 4, 8)
+    assert (p["tile_rows"], p["query_tiles"], p["key_tiles"]) == (128, 1032, 8)
+    assert (p["split_tiles"], p["workspace_bytes"]) == (0, 0)
+
+
+def test_short_underfilled_call_splits():
+    """Few 128-row tiles with many keys below the ping-pong threshold: 3
+    tiles on 512 slots are split along the keys."""
+    p = attn_plan(1, 1, 300, 1500, 128)
+    check_invariants(p, 1, 1, 300, 1500, 128, 256)
+    assert (p["tile_rows"], p["query_tiles"], p["split_tiles"]) == (128, 3, 3) and p["key_ranges"] >= 2
 
 
 @pytest.mark.parametrize("B,H,Sq,Skv,D,n_cu", [
@@ -66,7 +81,7 @@ def test_plan_invariants(B, H, Sq, Skv, D, n_cu):
 
 def test_single_key_tile_is_never_split():
     p = attn_plan(1, 1, 300, 64, 128)
-    assert (p["whole_tiles"], p["split_tiles"], p["key_ranges"]) == (2, 0, 0)
+    assert (p["tile_rows"], p["whole_tiles"], p["split_tiles"], p["key_ranges"]) == (128, 3, 0, 0)
 
 
 def test_empty_problem_plans_nothing():
