@@ -1598,17 +1598,26 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
 // issued before any of them is used, combined online (running max, sum and
 // weighted O), so the loop is not a chain of dependent memory accesses.
 // Key-range slices of the fixup: the waves of a workgroup take the same 64
-// (row, 4-dim) pairs, wave i merging key ranges i, i + kFixSlices, ...; the
+// (row, 4-dim) pairs, wave i merging key ranges i, i + slices, ...; the
 // first wave combines the slices' results (read through LDS) and stores.
-// Each lane then waits for one batch of partial loads instead of several in
-// turn, and the grid has kFixSlices times as many workgroups.
-constexpr int kFixSlices = 4;
+// A lane then waits for one batch of (at most 8) partial loads instead of
+// several in turn.  Tiles split into fewer than 9 ranges per context take
+// one slice: there the extra waves and the combine cost more than they save
+// (measured: 8 + 5 ranges 4.4 -> 5.3 us, 2 ranges 12.2 -> 27.7 us with four).
+constexpr int kFixSlices = 4;  // at most
+__host__ __device__ inline int fix_slices(const AttnPlan &pl)
+{
+    const int most = pl.seg > pl.seg2 ? pl.seg : pl.seg2;
+    const int s = (most + 7) / 8;
+    return s < 1 ? 1 : (s > kFixSlices ? kFixSlices : s);
+}
 
 template <bool OUT_F32>
 __global__ __launch_bounds__(64 * kFixSlices) void split_fixup_kernel(AttnArgs a_in, AttnPlan pl)
 {
     const int BM = pl.bm;
     constexpr int FB = 8;
+    const int n_sl = fix_slices(pl);  // == blockDim.x / 64
     __shared__ float red[2][kFixSlices - 1][6][64];
     const int per_row = a_in.D / 4;
     const int lane = threadIdx.x & 63;
@@ -1632,12 +1641,12 @@ __global__ __launch_bounds__(64 * kFixSlices) void split_fixup_kernel(AttnArgs a
         m = -INFINITY;
         s = 0.f;
         acc = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int c0 = slice; c0 < n; c0 += FB * kFixSlices) {
+        for (int c0 = slice; c0 < n; c0 += FB * n_sl) {
             float l[FB];
             f32x4 o[FB];
 #pragma unroll
             for (int k = 0; k < FB; ++k) {
-                const int c = c0 + k * kFixSlices;
+                const int c = c0 + k * n_sl;
                 const int64_t u = u0 + min(c, n - 1);
                 l[k] = c < n ? pl.ws_lse[u * BM + r] : -INFINITY;
                 o[k] = *reinterpret_cast<const f32x4 *>(pl.ws_o + (u * BM + r) * a.D + d);
@@ -1662,6 +1671,7 @@ __global__ __launch_bounds__(64 * kFixSlices) void split_fixup_kernel(AttnArgs a
     // The slices' results combined on the first wave (buffer i of red);
     // slice 0 always holds unit 0, so the common maximum is finite.
     auto combine = [&](int i, float &m, float &s, f32x4 &acc) {
+        if (n_sl == 1) return;
         if (slice > 0) {
             float *e = &red[i][slice - 1][0][lane];
             e[0] = m;
@@ -1671,23 +1681,21 @@ __global__ __launch_bounds__(64 * kFixSlices) void split_fixup_kernel(AttnArgs a
         }
         __syncthreads();
         if (slice == 0) {
-            float ms[kFixSlices];
-            ms[0] = m;
+            float mx = m;
 #pragma unroll
-            for (int t = 1; t < kFixSlices; ++t) ms[t] = red[i][t - 1][0][lane];
-            float mx = ms[0];
-#pragma unroll
-            for (int t = 1; t < kFixSlices; ++t) mx = fmaxf(mx, ms[t]);
+            for (int t = 1; t < kFixSlices; ++t)
+                if (t < n_sl) mx = fmaxf(mx, red[i][t - 1][0][lane]);
             const float w0 = expf(m - mx);
             s *= w0;
             acc *= w0;
 #pragma unroll
-            for (int t = 1; t < kFixSlices; ++t) {
-                const float w = expf(ms[t] - mx);
-                s += w * red[i][t - 1][1][lane];
+            for (int t = 1; t < kFixSlices; ++t)
+                if (t < n_sl) {
+                    const float w = expf(red[i][t - 1][0][lane] - mx);
+                    s += w * red[i][t - 1][1][lane];
 #pragma unroll
-                for (int k = 0; k < 4; ++k) acc[k] += w * red[i][t - 1][2 + k][lane];
-            }
+                    for (int k = 0; k < 4; ++k) acc[k] += w * red[i][t - 1][2 + k][lane];
+                }
             m = mx;
         }
     };
@@ -1925,8 +1933,8 @@ hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream, const Workspace 
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && pl.n_units > 0) {
         const int64_t pairs = (int64_t)(pl.n_tiles - pl.n_dp) * pl.bm * (D / 4);
-        hipLaunchKernelGGL(split_fixup_kernel<OUT_F32>, dim3((unsigned)((pairs + 63) / 64)), dim3(64 * kFixSlices),
-                           0, stream, a, pl);
+        hipLaunchKernelGGL(split_fixup_kernel<OUT_F32>, dim3((unsigned)((pairs + 63) / 64)),
+                           dim3(64 * fix_slices(pl)), 0, stream, a, pl);
         e = hipGetLastError();
     }
     if (ws != nullptr) {
