@@ -335,7 +335,7 @@ regenvc_status regenvc_cross_attn_dual_plan_query(int32_t B, int32_t H, int32_t 
                                                   regenvc_attn_plan *plan);
 
 /* Work plan of one regenvc_attn_partials_fwd call: query_tiles counts the
-   tiles of every chunk (num_chunks * B * H * ceil(Sq / 256)), key_tiles is
+   tiles of every chunk (num_chunks * B * H * ceil(Sq / tile_rows)), key_tiles is
    the last chunk's, and split tiles (the last ones of the launch) are split
    only when every chunk they belong to has that many key tiles.  Host-only;
    the chunk arguments as in regenvc_attn_partials_fwd. */

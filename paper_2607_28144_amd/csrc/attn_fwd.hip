@@ -1870,14 +1870,12 @@ int forced_schedule()
 // Kernel of a launch with n_kt key tiles per whole tile: the ping-pong
 // schedule from kPingPongMinTiles key tiles on, the paired interleaved one
 // below; dual-context launches always take the 8-wave interleaved kernel
-// (its parked first result needs the LDS), chunked ones never the paired.
-int pick_schedule(int n_kt, bool dual, bool chunked)
+// (its parked first result needs the LDS).
+int pick_schedule(int n_kt, bool dual)
 {
     if (dual) return kSchedInterleaved;
-    int s = forced_schedule();
-    if (s == 0) s = n_kt >= kPingPongMinTiles ? kSchedPingPong : kSchedPaired;
-    if (chunked && s == kSchedPaired) s = kSchedInterleaved;
-    return s;
+    const int s = forced_schedule();
+    return s != 0 ? s : n_kt >= kPingPongMinTiles ? kSchedPingPong : kSchedPaired;
 }
 
 // The work plan of launch `a` on n_cu compute units.
@@ -1949,7 +1947,7 @@ hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream, const Workspace 
 bool plan_attn(int B, int H, int Sq, int Skv, int D, int n_cu, AttnPlan *out, int Skv2)
 {
     if (B < 0 || H < 0 || Sq < 0 || Skv < 1 || n_cu < 1) return false;
-    const int sched = pick_schedule((int)(((int64_t)Skv + kBlockN - 1) / kBlockN), Skv2 > 0, false);
+    const int sched = pick_schedule((int)(((int64_t)Skv + kBlockN - 1) / kBlockN), Skv2 > 0);
     // paired launches: 128-row tiles, two resident per CU
     const int BM = sched == kSchedPaired ? 128 : kWaves * 32;
     const int slots = sched == kSchedPaired && n_cu <= 0x3fffffff ? 2 * n_cu : n_cu;
@@ -1970,17 +1968,19 @@ bool plan_attn(int B, int H, int Sq, int Skv, int D, int n_cu, AttnPlan *out, in
 
 bool plan_attn_chunks(int B, int H, int Sq, int n_chunks, const int32_t *clen, int D, int n_cu, AttnPlan *out)
 {
-    constexpr int BM = kWaves * 32;
     if (n_chunks < 1 || n_chunks > kMaxChunks || B < 0 || H < 0 || Sq < 0 || n_cu < 1) return false;
     for (int c = 0; c < n_chunks; ++c)
         if (clen[c] < 1) return false;
+    auto kt = [](int len) { return (int)(((int64_t)len + kBlockN - 1) / kBlockN); };
+    const int n_kt = kt(clen[n_chunks - 1]);
+    const int sched = pick_schedule(n_kt, false);
+    const int BM = sched == kSchedPaired ? 128 : kWaves * 32;
+    const int slots = sched == kSchedPaired && n_cu <= 0x3fffffff ? 2 * n_cu : n_cu;
     const int64_t n_qtiles = ((int64_t)Sq + BM - 1) / BM;
     const int64_t per_chunk = n_qtiles * H * B;
     if (n_qtiles * H > 0x7fffffff || per_chunk > 0x7fffffff / n_chunks) return false;
-    auto kt = [](int len) { return (int)(((int64_t)len + kBlockN - 1) / kBlockN); };
-    const int n_kt = kt(clen[n_chunks - 1]);
-    *out = make_plan((int)n_qtiles, (int)(per_chunk * n_chunks), n_kt, n_cu, D, BM);
-    out->sched = pick_schedule(n_kt, false, true);
+    *out = make_plan((int)n_qtiles, (int)(per_chunk * n_chunks), n_kt, slots, D, BM);
+    out->sched = sched;
     out->tiles_per_chunk = (int)per_chunk;
     if (out->n_units > 0 && per_chunk > 0) {
         // the split tiles are the last ones: their chunks must all have n_kt key tiles

@@ -332,13 +332,15 @@ def test_chunked_partials_plan_query(lib):
     plan = _lib.AttnPlan()
     b = (ctypes.c_int32 * 5)(0, 2730, 5460, 8190, 10920)
     expect(lib, lib.regenvc_attn_partials_plan_query(1, 5, 10920, 4, b, 128, 256, ctypes.byref(plan)), _lib.OK)
-    assert plan.query_tiles == 860 and plan.key_tiles == 43
+    assert plan.tile_rows == 256 and plan.query_tiles == 860 and plan.key_tiles == 43
     assert plan.whole_tiles == 768 and plan.split_tiles == 92 and plan.key_ranges >= 2
     assert plan.workspace_bytes == plan.split_tiles * plan.key_ranges * 256 * 129 * 4
-    # 72 tiles on 256 CUs: every tile is a split candidate, and chunk 0 has 1 key tile against 6
+    # short chunks (6 key tiles in the last): 128-row tiles, two per CU; 144 tiles on 512 slots are
+    # all split candidates, and chunk 0 has 1 key tile against 6
     b = (ctypes.c_int32 * 5)(5, 69, 70, 400, 777)
     expect(lib, lib.regenvc_attn_partials_plan_query(2, 3, 700, 4, b, 128, 256, ctypes.byref(plan)), _lib.OK)
-    assert plan.query_tiles == 72 and plan.split_tiles == 0 and plan.workspace_bytes == 0
+    assert plan.tile_rows == 128 and plan.query_tiles == 144 and plan.split_tiles == 0
+    assert plan.workspace_bytes == 0
     # equal key tile counts: the same tiles are split
     b = (ctypes.c_int32 * 4)(0, 3000, 6000, 9000)
     expect(lib, lib.regenvc_attn_partials_plan_query(1, 2, 1000, 3, b, 128, 256, ctypes.byref(plan)), _lib.OK)
