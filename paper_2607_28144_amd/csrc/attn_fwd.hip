@@ -1604,6 +1604,8 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
 // several in turn.  Tiles split into fewer than 9 ranges per context take
 // one slice: there the extra waves and the combine cost more than they save
 // (measured: 8 + 5 ranges 4.4 -> 5.3 us, 2 ranges 12.2 -> 27.7 us with four).
+// A workgroup holds 256 / (64 * slices) groups of 64 pairs (one for three
+// slices).
 constexpr int kFixSlices = 4;  // at most
 __host__ __device__ inline int fix_slices(const AttnPlan &pl)
 {
@@ -1611,19 +1613,21 @@ __host__ __device__ inline int fix_slices(const AttnPlan &pl)
     const int s = (most + 7) / 8;
     return s < 1 ? 1 : (s > kFixSlices ? kFixSlices : s);
 }
+__host__ __device__ inline int fix_groups(int slices) { return kFixSlices / slices; }
 
 template <bool OUT_F32>
 __global__ __launch_bounds__(64 * kFixSlices) void split_fixup_kernel(AttnArgs a_in, AttnPlan pl)
 {
     const int BM = pl.bm;
     constexpr int FB = 8;
-    const int n_sl = fix_slices(pl);  // == blockDim.x / 64
+    const int n_sl = fix_slices(pl), n_grp = fix_groups(n_sl);  // blockDim.x == 64 * n_sl * n_grp
     __shared__ float red[2][kFixSlices - 1][6][64];
     const int per_row = a_in.D / 4;
     const int lane = threadIdx.x & 63;
-    const int slice = threadIdx.x >> 6;
+    const int slice = (threadIdx.x >> 6) % n_sl, grp = (threadIdx.x >> 6) / n_sl;
+    const int entry = grp * (n_sl - 1) + slice - 1;  // this wave's LDS entry (slice > 0): < kFixSlices - 1
     const int64_t rows = (int64_t)(pl.n_tiles - pl.n_dp) * BM;
-    const int64_t pair = (int64_t)blockIdx.x * 64 + lane;
+    const int64_t pair = ((int64_t)blockIdx.x * n_grp + grp) * 64 + lane;
     // lanes past the last row merge the last one again (in bounds) and store nothing
     const int64_t row = min(pair / per_row, rows - 1);
     const int d = (int)(pair % per_row) * 4;
@@ -1673,7 +1677,7 @@ __global__ __launch_bounds__(64 * kFixSlices) void split_fixup_kernel(AttnArgs a
     auto combine = [&](int i, float &m, float &s, f32x4 &acc) {
         if (n_sl == 1) return;
         if (slice > 0) {
-            float *e = &red[i][slice - 1][0][lane];
+            float *e = &red[i][entry][0][lane];
             e[0] = m;
             e[64] = s;
 #pragma unroll
@@ -1682,19 +1686,20 @@ __global__ __launch_bounds__(64 * kFixSlices) void split_fixup_kernel(AttnArgs a
         __syncthreads();
         if (slice == 0) {
             float mx = m;
+            const int e0 = grp * (n_sl - 1) - 1;  // entry of slice t: e0 + t
 #pragma unroll
             for (int t = 1; t < kFixSlices; ++t)
-                if (t < n_sl) mx = fmaxf(mx, red[i][t - 1][0][lane]);
+                if (t < n_sl) mx = fmaxf(mx, red[i][e0 + t][0][lane]);
             const float w0 = expf(m - mx);
             s *= w0;
             acc *= w0;
 #pragma unroll
             for (int t = 1; t < kFixSlices; ++t)
                 if (t < n_sl) {
-                    const float w = expf(red[i][t - 1][0][lane] - mx);
-                    s += w * red[i][t - 1][1][lane];
+                    const float w = expf(red[i][e0 + t][0][lane] - mx);
+                    s += w * red[i][e0 + t][1][lane];
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) acc[k] += w * red[i][t - 1][2 + k][lane];
+                    for (int k = 0; k < 4; ++k) acc[k] += w * red[i][e0 + t][2 + k][lane];
                 }
             m = mx;
         }
@@ -1931,8 +1936,9 @@ hipError_t launch_attn_t(const AttnArgs &a, hipStream_t stream, const Workspace 
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && pl.n_units > 0) {
         const int64_t pairs = (int64_t)(pl.n_tiles - pl.n_dp) * pl.bm * (D / 4);
-        hipLaunchKernelGGL(split_fixup_kernel<OUT_F32>, dim3((unsigned)((pairs + 63) / 64)),
-                           dim3(64 * fix_slices(pl)), 0, stream, a, pl);
+        const int sl = fix_slices(pl), grp = fix_groups(sl);
+        hipLaunchKernelGGL(split_fixup_kernel<OUT_F32>, dim3((unsigned)((pairs + 64 * grp - 1) / (64 * grp))),
+                           dim3(64 * sl * grp), 0, stream, a, pl);
         e = hipGetLastError();
     }
     if (ws != nullptr) {
