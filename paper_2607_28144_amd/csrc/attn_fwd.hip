@@ -10,11 +10,13 @@
 // Work decomposition
 //   workgroup = 8 waves = one (batch, head, 256-query tile); one per CU, so
 //               each SIMD runs two waves and one wave's exponentials overlap
-//               the other's matrix instructions.
+//               the other's matrix instructions.  Short key ranges use 4-wave
+//               workgroups of 128 queries instead, two per CU ("paired").
 //   wave      = 32 queries, all head dims, every key tile.
 //   key tile  = 64 keys.  K and V tiles are copied HBM -> LDS with
 //               global_load_lds_dwordx4 (no register staging) into a ring of
-//               LDS stages (3 in the interleaved schedule, 4 in ping-pong).
+//               LDS stages (3 in the interleaved schedule, 4 in ping-pong,
+//               separate K and V rings of 2 when paired).
 //   Workgroups are renumbered so that the tiles of one head run on the same
 //   XCD (each XCD has its own L2; the hardware deals workgroups round-robin).
 //
@@ -30,7 +32,8 @@
 //   a joint permutation of keys and values, so no shuffle is needed.
 //
 // Two schedules of the key loop (the launch picks one by the number of key
-// tiles; results agree to rounding):
+// tiles; results agree to rounding; the interleaved one runs 8 waves or, in
+// pairs, 4):
 //   interleaved (attn_fwd_kernel), per wave and tile t:
 //     phase X:  MFMA  S_{t+1} = K_{t+1} Q^T   beside  VALU  softmax of S_t
 //     phase Y:  MFMA  O^T += V_t^T P_t^T       beside  the rest of it

@@ -226,6 +226,104 @@ __device__ __forceinline__ void tile_body(const ASrc &asrc, const Out &o, int ti
     }
 
     // epilogue: acc[nb][mb][i] = y[m0 + wm*WM + mb*16 + x][n0 + wn*16*NB + nb*16 + 4g + i]
+    constexpr bool BF16_OUT = EPI == kBias || EPI == kBiasGelu || EPI == kBiasSilu;
+    if constexpr (BF16_OUT) {
+        // A whole-width tile with 16-byte aligned rows goes out as full rows:
+        // the values are staged in the (now idle) LDS, row-major with 16-byte
+        // chunk c of row r at chunk c ^ (r & 15), and each store instruction
+        // then writes whole 16-byte chunks of consecutive rows instead of 8
+        // bytes of each of 16 rows.
+        if (n0 + BN <= o.N && (reinterpret_cast<uintptr_t>(o.out) & 15) == 0 && (o.ldo & 7) == 0) {
+            constexpr int CH = BN / 8;  // 16-byte chunks per staged row
+            static_assert(CH % 16 == 0 && (BM * CH) % kThreads == 0, "staging shape");
+            __syncthreads();  // every wave is done reading the ring
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+                const int n = n0 + wn * (16 * NB) + nb * 16 + 4 * g;
+                f32x4 bv = {0.f, 0.f, 0.f, 0.f};
+                if (o.bias != nullptr) {
+                    const uint64_t b4 = *reinterpret_cast<const uint64_t *>(o.bias + n);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) bv[i] = bf((uint16_t)(b4 >> (16 * i)));
+                }
+                const int c = wn * 2 * NB + nb * 2 + g / 2;
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) {
+                    const int r = wm * WM + mb * 16 + x;
+                    const f32x4 y = acc[nb][mb] + bv;
+                    bf16x4 w;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        w[i] = (__bf16)(EPI == kBiasGelu ? gelu_tanh(y[i]) : EPI == kBiasSilu ? silu(y[i]) : y[i]);
+                    *(__attribute__((address_space(3))) bf16x4 *)((lds_char *)smem + r * (BN * 2) +
+                                                                 ((c ^ (r & 15)) * 16) + (g & 1) * 8) = w;
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int it = 0; it < BM * CH / kThreads; ++it) {
+                const int id = it * kThreads + (int)threadIdx.x;
+                const int r = id / CH, c = id % CH;
+                const bf16x8 v = *(const lds_bf16x8 *)((const lds_char *)smem + r * (BN * 2) + ((c ^ (r & 15)) * 16));
+                if (m0 + r < o.M)
+                    *reinterpret_cast<bf16x8 *>(static_cast<uint16_t *>(o.out) + (int64_t)(m0 + r) * o.ldo + n0 +
+                                                c * 8) = v;
+            }
+            return;
+        }
+    }
+    if constexpr (EPI == kGatedRes) {
+        // The same for the read-modify-write of the fp32 residual, in two
+        // passes over half the tile's channels each (the staged fp32 half
+        // tile fits the LDS): y + bias is staged, and the lane that owns a
+        // 16-byte chunk of a row adds gate * y to it with whole-chunk loads
+        // and stores of consecutive rows.
+        if (n0 + BN <= o.N && (reinterpret_cast<uintptr_t>(o.out) & 15) == 0 && (o.ldo & 3) == 0) {
+            constexpr int HALF = BN / 2;  // channels per pass
+            constexpr int CH = HALF / 4;  // 16-byte chunks per staged row
+            constexpr int WCH = 16 * NB;  // channels of one wave column
+            static_assert(HALF % WCH == 0 && CH % 16 == 0 && (BM * CH) % kThreads == 0, "staging shape");
+#pragma unroll
+            for (int pass = 0; pass < 2; ++pass) {
+                __syncthreads();  // the ring (first pass) or the previous half is no longer read
+                if (wn * WCH / HALF == pass) {
+#pragma unroll
+                    for (int nb = 0; nb < NB; ++nb) {
+                        const int col = wn * WCH + nb * 16 + 4 * g;  // channel within the tile
+                        f32x4 bv = {0.f, 0.f, 0.f, 0.f};
+                        if (o.bias != nullptr) {
+                            const uint64_t b4 = *reinterpret_cast<const uint64_t *>(o.bias + n0 + col);
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) bv[i] = bf((uint16_t)(b4 >> (16 * i)));
+                        }
+                        const int c = (col - pass * HALF) / 4;
+#pragma unroll
+                        for (int mb = 0; mb < MB; ++mb) {
+                            const int r = wm * WM + mb * 16 + x;
+                            *(__attribute__((address_space(3))) f32x4 *)((lds_char *)smem + r * (HALF * 4) +
+                                                                        ((c ^ (r & 15)) * 16)) = acc[nb][mb] + bv;
+                        }
+                    }
+                }
+                __syncthreads();
+#pragma unroll 2
+                for (int it = 0; it < BM * CH / kThreads; ++it) {
+                    const int id = it * kThreads + (int)threadIdx.x;
+                    const int r = id / CH, c = id % CH;
+                    if (m0 + r >= o.M) continue;
+                    const int n = n0 + pass * HALF + c * 4;
+                    const f32x4 y =
+                        *(const __attribute__((address_space(3))) f32x4 *)((const lds_char *)smem + r * (HALF * 4) +
+                                                                         ((c ^ (r & 15)) * 16));
+                    const f32x4 gv = o.gate != nullptr ? *reinterpret_cast<const f32x4 *>(o.gate + n)
+                                                       : f32x4{1.f, 1.f, 1.f, 1.f};
+                    f32x4 *p = reinterpret_cast<f32x4 *>(static_cast<float *>(o.out) + (int64_t)(m0 + r) * o.ldo + n);
+                    *p = *p + gv * y;
+                }
+            }
+            return;
+        }
+    }
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
         const int n = n0 + wn * (16 * NB) + nb * 16 + 4 * g;
@@ -260,11 +358,14 @@ __device__ __forceinline__ void tile_body(const ASrc &asrc, const Out &o, int ti
     }
 }
 
-// LDS bytes of a BM x (16 NB WN) tile's double-buffered ring.
+// LDS bytes of a BM x (16 NB WN) tile: its double-buffered ring, or the
+// bf16 output staging if that is larger.
 template <int BM, int WN, int NB = 4>
 constexpr int lds_bytes()
 {
-    return 2 * (BM + 16 * NB * WN) * kRowBytes;
+    constexpr int ring = 2 * (BM + 16 * NB * WN) * kRowBytes;
+    constexpr int staging = BM * 16 * NB * WN * 2;  // bf16 tile, or half of it in fp32
+    return ring > staging ? ring : staging;
 }
 
 // XCD-aware tile count helpers for the launchers.
