@@ -1581,17 +1581,28 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
             return;
         }
     }
-    // A split tile's key range: its normalized partial to the workspace.
+    // A split tile's key range: its normalized partial (f32) to the
+    // workspace, staged in the ring and written as full rows like a whole
+    // tile's f32 output, and its LSE.
+    __syncthreads();  // every wave is done with the ring
+    lds_char *stg = (lds_char *)smem + wave * 32 * D * 4;
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
         const float lt = quad_sum(lsum[qb]);
         const float inv = 1.0f / quad_sum(rsum[qb]);
         const int qrow = qrow0_e + qb * 16, qi = qi0_e + qb * 16;
-        if (qi >= a.Sq) continue;
-        float *orow = pl.ws_o + ((int64_t)slot * BM + qrow) * D;
+        if (g_e == 0 && qi < a.Sq) pl.ws_lse[(int64_t)slot * BM + qrow] = (mref[qb] + __log2f(lt)) * kLn2;
 #pragma unroll
-        for (int db = 0; db < DB; ++db) *reinterpret_cast<f32x4 *>(orow + db * 16 + g_e * 4) = oacc[db][qb] * inv;
-        if (g_e == 0) pl.ws_lse[(int64_t)slot * BM + qrow] = (mref[qb] + __log2f(lt)) * kLn2;
+        for (int db = 0; db < DB; ++db) stage_out4_f32<D>(stg, qb * 16 + x_e, db * 16 + g_e * 4, oacc[db][qb] * inv);
+    }
+    constexpr int CPR = D / 4;     // 16-byte chunks per row
+    constexpr int RPI = 64 / CPR;  // rows per store instruction
+#pragma unroll
+    for (int it = 0; it < 32 / RPI; ++it) {
+        const int r = it * RPI + lane_e / CPR, c = lane_e % CPR;
+        const f32x4 w = *(const __attribute__((address_space(3))) f32x4 *)(stg + r * D * 4 + (c ^ (r & (CPR - 1))) * 16);
+        if (qt * BM + wave * 32 + r < a.Sq)
+            *reinterpret_cast<f32x4 *>(pl.ws_o + ((int64_t)slot * BM + wave * 32 + r) * D + c * 4) = w;
     }
 }
 
