@@ -613,9 +613,9 @@ __device__ __forceinline__ void wait_vmcnt()
 
 // ACC: the ring-accumulate epilogue; DUAL: two contexts summed (each a
 // separate instantiation, so that the plain kernels keep their register
-// allocation).  A dual launch runs the key pipeline twice over one set of Q
-// fragments: first context, then, with the first result parked in LDS as
-// bf16 (the precision of a single context-attention output), the second.
+// allocation).  A dual launch runs the key pipeline twice over one query
+// tile: first context, then, with the first result parked in LDS as bf16
+// (the precision of a single context-attention output), the second.
 template <int D, bool OUT_F32, bool ACC, bool DUAL = false, int WAVES = kWaves>
 __global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_kernel(AttnArgs a_in, AttnPlan pl)
@@ -682,7 +682,22 @@ void attn_fwd_kernel(AttnArgs a_in, AttnPlan pl)
     // lsum): one over the work item's key range, or (dual launches, whole
     // tiles) one over each context.
     const int n_pass = DUAL && slot < 0 ? 2 : 1;
-    for (int ps = 0; ps < n_pass; ++ps) {
+    // unrolled for dual launches: each pass then gets its own register
+    // allocation (as a loop, the state carried between the passes spilled)
+#pragma unroll
+    for (int ps = 0; ps < (DUAL ? 2 : 1); ++ps) {
+    if (ps >= n_pass) break;
+    if (DUAL && ps == 1) {
+        // the second pass reads its Q fragments again (from L2, as a rule)
+        // rather than keeping them live through the first pass's epilogue
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds) {
+            if (qi < Sq)
+                qf[ds] = *reinterpret_cast<const bf16x8 *>(qp + (int64_t)qi * a.q_ss + ds * 16 + hi * 8);
+            else
+                qf[ds] = bf16x8{};
+        }
+    }
     const KvSrc src = (DUAL && (slot >= 0 ? wi.src : ps) == 1) ? src1 : src0;
     const int kt0 = wi.kt0;
     const int kt1 = DUAL && slot < 0 ? src.n_kt : wi.kt1;
