@@ -73,8 +73,11 @@ def bits(rng, shape, scale=1.0):
 
 
 @pytest.mark.parametrize("M,N,K", [(300, 256, 1536), (1000, 1536, 1536), (577, 4608, 1536), (333, 1536, 8960),
-                                   (10920, 1536, 1536)])
+                                   (10920, 1536, 1536), (500, 400, 512), (289, 272, 64)])
 def test_linear_epilogues(M, N, K):
+    """Whole-width tiles stage their output through LDS; a last tile column
+    narrower than 256 channels (N = 400, 272) stores straight from the
+    accumulators."""
     rng = np.random.default_rng(M + N + K)
     a, w, b = bits(rng, (M, K)), bits(rng, (N, K), 0.02), bits(rng, (N,), 0.02)
     gate = rng.standard_normal(N).astype(np.float32)
