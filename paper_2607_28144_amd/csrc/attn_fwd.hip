@@ -1102,16 +1102,15 @@ void attn_fwd_kernel(AttnArgs a_in, AttnPlan pl)
     const float inv = 1.0f / pair_sum(rsum);
     const float lse_last = (mref + __log2f(lt)) * kLn2;
     if constexpr (DUAL) {
-        // the sum goes out straight from the accumulator layout (measured
-        // faster here than staging it for full-row stores)
         if (hi == 0 && qi < Sq) {
             const int64_t li = ((int64_t)b * a.H + h) * a.Sq + qi;
             if (a.lse != nullptr) a.lse[li] = lse1;
             if (a.lse2 != nullptr) a.lse2[li] = lse_last;
         }
-        if (qi >= Sq) return;
+        // the sum, staged in the (now idle) ring and written as full rows
         const lds_char *park = (const lds_char *)smem + G::LDS + threadIdx.x * 16;
-        char *orow = static_cast<char *>(a.o) + ((int64_t)b * a.o_sb + (int64_t)qi * a.o_ss + (int64_t)h * a.o_sh) * 2;
+        __syncthreads();  // every wave is done with the ring
+        lds_char *stg = (lds_char *)smem + wave * 32 * D * 2;
 #pragma unroll
         for (int j = 0; j < DB * 2; ++j) {
             const bf16x8 o1 = *(const lds_bf16x8 *)(park + j * THREADS * 16);
@@ -1121,9 +1120,10 @@ void attn_fwd_kernel(AttnArgs a_in, AttnPlan pl)
                 bf16x4 w;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) w[e] = (__bf16)(oacc[db][gq * 4 + e] * inv + (float)o1[half * 4 + e]);
-                *reinterpret_cast<bf16x4 *>(orow + (db * 32 + gq * 8 + hi * 4) * 2) = w;
+                stage_out4<D>(stg, col, db * 32 + gq * 8 + hi * 4, w);
             }
         }
+        store_staged_rows<D>(a, stg, lane, b, h, qt * BM + wave * 32);
         return;
     } else {
 #pragma unroll
