@@ -57,12 +57,17 @@
  *   - All entry points are reentrant; concurrent calls on different streams
  *     are independent.
  *   - The same launch configuration gives bit-identical results run to run.
- *   - Two schedules of the attention kernel exist; a launch whose key range
- *     spans at least 32 tiles of 64 keys uses the ping-pong one, a shorter
- *     one the interleaved one.  They compute the same quantities with a
- *     different summation order (results agree to rounding, not bitwise).
- *     The environment variable REGENVC_ATTN_SCHEDULE=pingpong|interleaved,
- *     read at each call, forces one of them (diagnostics and tests).
+ *   - Three forms of the attention kernel exist; a launch whose key range
+ *     spans at least 32 tiles of 64 keys uses the ping-pong one (256-query
+ *     tiles), a shorter one the interleaved one in pairs (128-query tiles,
+ *     two workgroups per compute unit), a dual cross-attention the 8-wave
+ *     interleaved one (256-query tiles).  The ping-pong and interleaved
+ *     kernels compute the same quantities with a different summation order
+ *     (results agree to rounding, not bitwise); the paired and 8-wave
+ *     interleaved forms agree bitwise row by row.  The environment variable
+ *     REGENVC_ATTN_SCHEDULE=pingpong|interleaved|paired, read at each call,
+ *     forces one of them (diagnostics and tests; the dual call honours only
+ *     interleaved).
  */
 #ifndef REGENVC_ATTN_H
 #define REGENVC_ATTN_H

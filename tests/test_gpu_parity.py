@@ -419,6 +419,30 @@ def test_schedule_window_rows(schedule):
                      lse.cpu().numpy()[:, hh:hh + 1][:, :, rows], l_ref)
 
 
+def test_paired_and_eight_wave_interleaved_agree_bitwise(monkeypatch):
+    """The paired kernel (4-wave workgroups of 128 queries) runs the 8-wave
+    interleaved kernel's per-row arithmetic: on a shape that both plans cover
+    in whole rounds without splitting (H=4, 16384 queries: 256 tiles of 256,
+    512 of 128; 512 context tokens), O and LSE are bitwise equal; both match
+    the oracle on sampled rows."""
+    B, H, S, Skv, D = 1, 4, 16384, 512, 128
+    q, k, v = synth.qkv(61, B, H, S, Skv, D)
+    dq, dk, dv = dev(q), dev(k), dev(v)
+    res = {}
+    for sched in ("paired", "interleaved"):
+        monkeypatch.setenv("REGENVC_ATTN_SCHEDULE", sched)
+        plan = api().attn_plan(B, H, S, Skv, D, torch.cuda.get_device_properties(0).multi_processor_count)
+        assert plan["split_tiles"] == 0 and plan["tile_rows"] == (128 if sched == "paired" else 256), plan
+        res[sched] = api().attn_fwd(dq, dk, dv)
+        torch.cuda.synchronize()
+    assert torch.equal(res["paired"][0], res["interleaved"][0])
+    assert torch.equal(res["paired"][1], res["interleaved"][1])
+    rows = sample_rows(S, 40, 62)
+    o_ref, l_ref = oracle.attn(np.ascontiguousarray(q[:, rows]), k, v, synth.default_scale(D))
+    assert_close("paired = interleaved, sampled rows", host(res["paired"][0])[:, rows], o_ref,
+                 res["paired"][1].cpu().numpy()[:, :, rows], l_ref)
+
+
 # ------------------------------------------------------------------ partial + merge
 def _partials(q, k, v, bounds, scale):
     dq = dev(q)
