@@ -148,18 +148,32 @@ __global__ __launch_bounds__(256) void rms_norm_kernel(RmsNormArgs a)
 // Vector form (C a multiple of 8, 16-byte aligned rows and e): each wave
 // takes kModRows consecutive rows; a lane walks 8-channel chunks, forms
 // silu(e) of a chunk once and applies it to the chunk of every one of its
-// rows (16-byte weight loads, kModRows in flight).
+// rows (16-byte weight loads, all of a lane's issued before the first is
+// used; C <= 2048).
 constexpr int kModRows = 4;
 
 __global__ __launch_bounds__(256) void modulation_vec_kernel(ModulationArgs a)
 {
+    constexpr int kIt = 4;  // 512-channel steps per lane: C <= 2048
     const int lane = threadIdx.x & 63;
     const int j0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kModRows;
     if (j0 >= a.rows) return;
     const int nr = min(kModRows, a.rows - j0);
     const uint16_t *w = static_cast<const uint16_t *>(a.w) + (int64_t)j0 * a.C;
+    // every weight chunk of this lane is requested before the first is used
+    bf16x8 v[kIt][kModRows];
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) {
+        const int c = lane * 8 + it * 512;
+#pragma unroll
+        for (int r = 0; r < kModRows; ++r)
+            if (c < a.C && r < nr) v[it][r] = *reinterpret_cast<const bf16x8 *>(w + (int64_t)r * a.C + c);
+    }
     float s[kModRows] = {};
-    for (int c = lane * 8; c < a.C; c += 64 * 8) {
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) {
+        const int c = lane * 8 + it * 512;
+        if (c >= a.C) break;
         const f32x4 e0 = *reinterpret_cast<const f32x4 *>(a.e + c);
         const f32x4 e1 = *reinterpret_cast<const f32x4 *>(a.e + c + 4);
         float u[8];
@@ -171,9 +185,8 @@ __global__ __launch_bounds__(256) void modulation_vec_kernel(ModulationArgs a)
 #pragma unroll
         for (int r = 0; r < kModRows; ++r) {
             if (r < nr) {
-                const bf16x8 v = *reinterpret_cast<const bf16x8 *>(w + (int64_t)r * a.C + c);
 #pragma unroll
-                for (int i = 0; i < 8; ++i) s[r] = fmaf((float)v[i], u[i], s[r]);
+                for (int i = 0; i < 8; ++i) s[r] = fmaf((float)v[it][r][i], u[i], s[r]);
             }
         }
     }
@@ -280,7 +293,7 @@ hipError_t launch_rms_norm(const RmsNormArgs &a, hipStream_t stream)
 
 hipError_t launch_modulation(const ModulationArgs &a, hipStream_t stream)
 {
-    const bool vec = a.C % 8 == 0 && ((uintptr_t)a.w & 15) == 0 && ((uintptr_t)a.e & 15) == 0;
+    const bool vec = a.C % 8 == 0 && a.C <= 2048 && ((uintptr_t)a.w & 15) == 0 && ((uintptr_t)a.e & 15) == 0;
     if (vec) {
         const int per_block = 4 * kModRows;
         hipLaunchKernelGGL(modulation_vec_kernel, dim3((unsigned)((a.rows + per_block - 1) / per_block)), dim3(256), 0,
