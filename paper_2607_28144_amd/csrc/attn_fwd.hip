@@ -1218,10 +1218,15 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
                 qf[qb][ks] = bf16x8{};
         }
 
-    // HBM -> LDS copies, as in the interleaved kernel: tiles in order kt0,
-    // kt0+1, ... (one call per tile, into ring stages 0, 1, 2, ...), the last
-    // one repeated into otherwise unused stages, so that every call issues
-    // exactly PER_TILE copies per thread and the vmcnt waits count tiles.
+    // HBM -> LDS copies: tiles in order kt0, kt0+1, ... into ring stages 0,
+    // 1, 2, ...; every tile is PER_TILE copies per thread, in two halves, K
+    // (LOADS copies) and V (LOADS copies), issued at different points of the
+    // schedule; advance_copy moves on to the next tile once both are out.
+    // Past the last tile the copies repeat it into stages that are not read
+    // again (every tile issues PER_TILE copies, so the vmcnt waits count
+    // tiles); the schedule's tail asks for none.
+    using T_ = std::true_type;
+    using F_ = std::false_type;
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_char *)smem;
     uint32_t kofs[LOADS], vofs[LOADS];
 #pragma unroll
@@ -1237,13 +1242,13 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
     int st_copy = 0;
     const uint16_t *kb_copy = kp + kt0 * k_step;
     const uint16_t *vb_copy = vp + kt0 * v_step;
-    auto issue_next = [&]() __attribute__((always_inline)) {
-        const uint32_t kdst = lds0 + st_copy * G::STAGE;
-        const uint32_t vdst = kdst + G::TILE;
+    auto issue_half = [&](auto is_v) __attribute__((always_inline)) {
+        constexpr bool V = decltype(is_v)::value;
+        const uint32_t dst = lds0 + st_copy * G::STAGE + (V ? G::TILE : 0);
         if (a.kv_off32 && tl_copy <= last_full) {
             const uint32_t blk = __builtin_amdgcn_readfirstlane(wave * LOADS * 1024);
-            lds_dma16_group<LOADS>(uniform_ptr(kb_copy), kofs, __builtin_amdgcn_readfirstlane(kdst) + blk);
-            lds_dma16_group<LOADS>(uniform_ptr(vb_copy), vofs, __builtin_amdgcn_readfirstlane(vdst) + blk);
+            lds_dma16_group<LOADS>(uniform_ptr(V ? vb_copy : kb_copy), V ? vofs : kofs,
+                                   __builtin_amdgcn_readfirstlane(dst) + blk);
         } else {
             const int key0 = tl_copy * kBlockN;
             const int last = Skv - 1 - key0;
@@ -1253,10 +1258,14 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
                 const int slot16 = blk * 64 + lane;
                 const int row = slot16 / NCH, phys = slot16 % NCH;
                 const int64_t key = key0 + min(row, last);
-                lds_dma16(kp + key * a.k_ss + k_slot<NCH>(row, phys) * 8, kdst + blk * 1024);
-                lds_dma16(vp + key * a.v_ss + v_slot<NCH>(row, phys) * 8, vdst + blk * 1024);
+                if (V)
+                    lds_dma16(vp + key * a.v_ss + v_slot<NCH>(row, phys) * 8, dst + blk * 1024);
+                else
+                    lds_dma16(kp + key * a.k_ss + k_slot<NCH>(row, phys) * 8, dst + blk * 1024);
             }
         }
+    };
+    auto advance_copy = [&]() __attribute__((always_inline)) {
         st_copy = st_copy == kStagesPP - 1 ? 0 : st_copy + 1;
         if (tl_copy < kt1 - 1) {
             ++tl_copy;
@@ -1415,8 +1424,6 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
         rsum[1] += r_sum[1];
     };
 
-    using T_ = std::true_type;
-    using F_ = std::false_type;
     auto st = [](int u) { return u & (kStagesPP - 1); };  // ring stage of the work item's tile u
     auto key0 = [&](int u) { return (kt0 + u) * kBlockN; };
     auto vlast = [&](int u) __attribute__((always_inline)) {  // V phase of the last (possibly ragged) tile
@@ -1447,15 +1454,22 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
     };
 
     // Prologue: tiles 0 and 1 in flight, tile 0 landed.
-    issue_next();
-    issue_next();
+    issue_half(F_{});
+    issue_half(T_{});
+    advance_copy();
+    issue_half(F_{});
+    issue_half(T_{});
+    advance_copy();
     wait_vmcnt<PER_TILE>();
     __syncthreads();
 
     // Interval pairs u = 0..T, two barriers each (the same count in both
     // groups).  Group 0 runs M(u) | V(u), group 1 runs V(u-1) | M(u).  Each
-    // wave copies tile u+2 right after its M(u) (stage of tile u-2, last read
-    // by PV(u-2) in pair u-1) and, before the barrier that ends pair u, waits
+    // wave copies its part of tile u+2 in pair u (stage of tile u-2, last
+    // read by PV(u-2) in pair u-1): the K half right after its M(u), the V
+    // half at the start of its V interval of pair u (so that the two halves'
+    // issue, which the CU's address unit serializes, is shared between the M
+    // and the V interval).  Before the barrier that ends pair u, a wave waits
     // for its copies of tile u+1, which M(u+1) reads after that barrier.  The
     // fragments an M phase starts with are read before the barrier ahead of
     // it: V fragments of its tile u-1, which landed a pair earlier and is not
@@ -1469,12 +1483,14 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
         __builtin_amdgcn_s_setprio(1);
         mphase(st(0), st(0), F_{}, T_{});
         __builtin_amdgcn_s_setprio(0);
-        issue_next();
+        issue_half(F_{});
         phase_barrier();
+        issue_half(T_{});
         if (T == 1)
             vlast(0);
         else
             vphase(key0(0), F_{});
+        advance_copy();
         wait_vmcnt<PER_TILE>();
         mprefetch(st(1), st(0), T_{});
         phase_barrier();
@@ -1482,9 +1498,11 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
             __builtin_amdgcn_s_setprio(1);
             mphase(st(u), st(u - 1), T_{}, T_{});
             __builtin_amdgcn_s_setprio(0);
-            issue_next();
+            issue_half(F_{});
             phase_barrier();
+            issue_half(T_{});
             vphase(key0(u), F_{});
+            advance_copy();
             wait_vmcnt<PER_TILE>();
             mprefetch(st(u + 1), st(u), T_{});
             phase_barrier();
@@ -1493,10 +1511,9 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
             __builtin_amdgcn_s_setprio(1);
             mphase(st(T - 1), st(T - 2), T_{}, T_{});
             __builtin_amdgcn_s_setprio(0);
-            issue_next();
             phase_barrier();
             vlast(T - 1);
-            wait_vmcnt<PER_TILE>();
+            wait_vmcnt<0>();  // (left in flight: the repeat copy of the pair before)
             mprefetch(st(T), st(T - 1), T_{});
             phase_barrier();
         }
@@ -1507,23 +1524,28 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
         end_barrier();
         end_barrier();
     } else {
+        // (the V half of a tile goes out a whole interval before its K half)
         __asm__ volatile("; group 1 schedule");
         mprefetch(st(0), st(0), F_{});
+        issue_half(T_{});
         phase_barrier();
         __builtin_amdgcn_s_setprio(1);
         mphase(st(0), st(0), F_{}, T_{});
         __builtin_amdgcn_s_setprio(0);
-        issue_next();
+        issue_half(F_{});
+        advance_copy();
         wait_vmcnt<PER_TILE>();
         phase_barrier();
         for (int u = 1; u < T; ++u) {
+            issue_half(T_{});
             vphase(key0(u - 1), F_{});
             mprefetch(st(u), st(u - 1), T_{});
             phase_barrier();
             __builtin_amdgcn_s_setprio(1);
             mphase(st(u), st(u - 1), T_{}, T_{});
             __builtin_amdgcn_s_setprio(0);
-            issue_next();
+            issue_half(F_{});
+            advance_copy();
             wait_vmcnt<PER_TILE>();
             phase_barrier();
         }
@@ -1534,11 +1556,9 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
         __asm__ volatile("; last M phase, group 1");
         mphase(st(T), st(T - 1), T_{}, F_{});
         __builtin_amdgcn_s_setprio(0);
-        issue_next();
-        wait_vmcnt<PER_TILE>();
         end_barrier();
     }
-    wait_vmcnt<0>();  // the clamped trailing copies must land before the workgroup exits
+    wait_vmcnt<0>();  // the repeat copies past the last tile must land before the workgroup exits
 
     // The epilogue's lane indices come from a fresh copy of the thread index
     // (opaque to the compiler), so that no index or address computed before
