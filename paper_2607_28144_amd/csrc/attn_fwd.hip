@@ -126,6 +126,20 @@ template <int NCH>
 __device__ __forceinline__ int k_slot(int row, int ch) { return ch ^ (row & (NCH - 1)); }
 template <int NCH>
 __device__ __forceinline__ int v_slot(int row, int ch) { return ch ^ ((4 * (row & 3)) & (NCH - 1)); }
+// V placement of the ping-pong kernel, whose transposing reads take 4
+// consecutive rows x 2 adjacent chunks per 16 lanes but rows 4g.. for lane
+// group g, so that two 16-lane groups read the same bank columns under the
+// XOR above.  With d = 128 the extra XOR of 2 (rows 4-11 of every 16) moves
+// groups 1 and 2 to the other half of the banks: any two of the four groups
+// that differ in one index bit then read 16 distinct chunks together.
+template <int NCH>
+__device__ __forceinline__ int vp_slot(int row, int ch)
+{
+    if constexpr (NCH == 16)
+        return ch ^ (4 * (row & 3) + 2 * (((row >> 2) ^ (row >> 3)) & 1));
+    else
+        return v_slot<NCH>(row, ch);
+}
 
 // The copies below name M0 as clobbered: they set it to the LDS destination,
 // and the compiler must not keep a value of its own there across them.  Clang
@@ -1234,7 +1248,7 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
         const int slot16 = (wave * LOADS + j) * 64 + lane;
         const int row = slot16 / NCH, phys = slot16 % NCH;
         kofs[j] = (uint32_t)((row * a.k_ss + k_slot<NCH>(row, phys) * 8) * 2);
-        vofs[j] = (uint32_t)((row * a.v_ss + v_slot<NCH>(row, phys) * 8) * 2);
+        vofs[j] = (uint32_t)((row * a.v_ss + vp_slot<NCH>(row, phys) * 8) * 2);
     }
     const int64_t k_step = (int64_t)kBlockN * a.k_ss, v_step = (int64_t)kBlockN * a.v_ss;
     const int last_full = Skv / kBlockN - 1;  // last tile with kBlockN keys
@@ -1259,7 +1273,7 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
                 const int row = slot16 / NCH, phys = slot16 % NCH;
                 const int64_t key = key0 + min(row, last);
                 if (V)
-                    lds_dma16(vp + key * a.v_ss + v_slot<NCH>(row, phys) * 8, dst + blk * 1024);
+                    lds_dma16(vp + key * a.v_ss + vp_slot<NCH>(row, phys) * 8, dst + blk * 1024);
                 else
                     lds_dma16(kp + key * a.k_ss + k_slot<NCH>(row, phys) * 8, dst + blk * 1024);
             }
@@ -1290,7 +1304,7 @@ void attn_fwd_pingpong_kernel(AttnArgs a_in, AttnPlan pl)
     for (int db = 0; db < DB; ++db) {
         const int row = 4 * g + (x >> 2);
         const int dcol = db * 16 + 4 * (x & 3);
-        voff[db] = G::TILE + (row * D + v_slot<NCH>(row, dcol >> 3) * 8 + (dcol & 7)) * 2;
+        voff[db] = G::TILE + (row * D + vp_slot<NCH>(row, dcol >> 3) * 8 + (dcol & 7)) * 2;
     }
     constexpr int NK = 4 * KS;  // K fragments per tile (each feeds two MFMAs)
     constexpr int NV = 2 * DB;  // V^T fragments per tile (each feeds two MFMAs)
