@@ -433,7 +433,7 @@ def main():
                     help="untimed steps: the shader clock takes ~60 window self-attention calls (~40 ms) under "
                          "load to settle, and calls within that time run up to 30 %% slower")
     ap.add_argument("--only", choices=["self", "cross", "share", "ring", "dual", "cross2", "copy", "normrope",
-                                       "block", "vae"],
+                                       "block", "vae", "configs"],
                     default=None,
                     help="time one component alone (for profiling); 'copy' runs a plain 1 GiB elementwise "
                          "copy kernel, the reference for scaling HBM byte counters; 'normrope' times the q/k "
@@ -441,7 +441,9 @@ def main():
                          "of the attention step); 'ring' runs the share with the merge fused into each chunk "
                          "(first chunk's partial, then ring-accumulate steps, the last into bf16); 'dual' "
                          "times the text (512) + image (257) cross-attention summed in one call, 'cross2' the "
-                         "same two contexts as two separate cross-attention calls (without the sum)")
+                         "same two contexts as two separate cross-attention calls (without the sum); "
+                         "'configs' the image-scale self-attention (S=4096) and the paper's own rank share "
+                         "(H=3, Sq=5460, 2 chunks), each alone")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle sample")
     args = ap.parse_args()
@@ -467,6 +469,12 @@ def main():
         return
     if args.only == "block":
         print(json.dumps({"dit_block_c5": dit_block_leg(torch, dev, args.steps, args.warmup)}), flush=True)
+        return
+    if args.only == "configs":
+        def to_dev(bits):
+            return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+        print(json.dumps(config_legs(torch, api, synth, dev, to_dev, args.steps, args.warmup)), flush=True)
         return
     if args.only == "vae":
         print(json.dumps({"split_vae_tile": vae_leg(torch, dev, args.steps, args.warmup)}), flush=True)
