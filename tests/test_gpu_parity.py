@@ -355,7 +355,10 @@ def schedule(request, monkeypatch):
 
 @pytest.mark.parametrize("Sq,Skv,D,out", [
     (1, 1, 128, "f32"), (65, 127, 128, "bf16"), (255, 257, 64, "bf16"), (300, 1000, 128, "f32"),
-    (513, 1, 64, "bf16"), (257, 2730, 128, "f32")])
+    (513, 1, 64, "bf16"), (257, 2730, 128, "f32"),
+    # 3 and 4 key tiles: the ping-pong ring (4 stages) just filled, and the
+    # tail of its schedule right after the loop's first pair
+    (70, 129, 128, "bf16"), (130, 256, 64, "f32"), (64, 200, 128, "f32")])
 def test_schedule_ragged_shapes(schedule, Sq, Skv, D, out):
     dt = torch.float32 if out == "f32" else torch.bfloat16
     run_and_check(f"{schedule} Sq={Sq} Skv={Skv} D={D} {out}", 2, 2, Sq, Skv, D, 200 + Sq + Skv, dt)
