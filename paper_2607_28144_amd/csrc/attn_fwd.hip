@@ -1804,9 +1804,13 @@ __global__ __launch_bounds__(64 * kFixSlices) void split_fixup_kernel(AttnArgs a
 // split unit costs its key range + 1.5 (the partial store), and the partials'
 // write + read traffic is priced at 5 TB/s against ~1 us per iteration.
 // n_cu counts workgroup slots: in paired launches (128-row tiles) two per
-// CU; there the tiles of a last, partial round that leaves each of them a
-// CU of its own run at about 0.65 of the paired time, and a split adds the
-// fixup launch (~2 iterations).
+// CU.  In a paired launch that does not fill one round, tiles that get a CU
+// of their own run at about 0.65 of the paired time, and a split adds the
+// fixup launch (~2 iterations).  After full rounds the leftover tiles start
+// only as the last round drains, so they cost a whole tile each, and the
+// fixup runs back to back with the attention kernel (measured on the window
+// cross-attention, 1032 tiles of 8 key tiles on 512 slots: 8 leftover
+// tiles split into 64 one-tile ranges, 53.5 -> 52.5 us).
 AttnPlan make_plan(int n_qtiles, int n_tiles, int n_kt, int n_cu, int D, int BM)
 {
     const bool paired = BM != kWaves * 32;
@@ -1821,7 +1825,8 @@ AttnPlan make_plan(int n_qtiles, int n_tiles, int n_kt, int n_cu, int D, int BM)
     const double whole = n_kt + 1.0;
     const int rounds = n_tiles / n_cu;
     const int rem = n_tiles - rounds * n_cu;
-    const double tail = rem == 0 ? 0.0 : (paired && rem <= n_cu / 2 ? 0.65 : 1.0) * whole;
+    const bool lone = paired && rounds == 0;  // an underfilled paired launch
+    const double tail = rem == 0 ? 0.0 : (lone && rem <= n_cu / 2 ? 0.65 : 1.0) * whole;
     double best = rounds * whole + tail;
     if (rem == 0 || n_kt < 2) return pl;
     for (int seg = 2; seg <= n_kt && seg <= 256; ++seg) {
@@ -1830,7 +1835,7 @@ AttnPlan make_plan(int n_qtiles, int n_tiles, int n_kt, int n_cu, int D, int BM)
         const int64_t sk_rounds = (units + n_cu - 1) / n_cu;
         const int len = (n_kt + seg - 1) / seg;
         const double traffic = 2.0 * units * BM * (D + 1) * 4 / 5e12 / 1e-6;
-        const double cost = rounds * whole + sk_rounds * (len + 1.5) + traffic + (paired ? 2.0 : 0.0);
+        const double cost = rounds * whole + sk_rounds * (len + 1.5) + traffic + (lone ? 2.0 : 0.0);
         if (cost < best) {
             best = cost;
             pl.n_dp = rounds * n_cu;

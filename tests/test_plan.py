@@ -54,12 +54,15 @@ def test_share_plan_splits_nothing():
 
 def test_cross_plan():
     """Cross-attention to 512 context tokens: 8 key tiles, so 128-row tiles
-    two per CU; the 1032 tiles are two rounds of 512 plus 8, which run whole
-    (each with a CU to itself) rather than split with a fixup launch."""
+    two per CU; the 1032 tiles are two rounds of 512 plus 8, and those 8
+    start only as the second round drains: each is split into 8 one-tile key
+    ranges (64 units) and recombined by the fixup."""
     p = attn_plan(1, 12, 10920, 512, 128)
     check_invariants(p, 1, 12, 10920, 512, 128, 256)
     assert (p["tile_rows"], p["query_tiles"], p["key_tiles"]) == (128, 1032, 8)
-    assert (p["split_tiles"], p["workspace_bytes"]) == (0, 0)
+    assert (p["whole_tiles"], p["split_tiles"], p["key_ranges"]) == (1024, 8, 8)
+    # partials: 64 units x 128 rows x (128 O + 1 LSE) floats
+    assert p["workspace_bytes"] == 64 * 128 * 129 * 4
 
 
 def test_short_underfilled_call_splits():
