@@ -1713,10 +1713,15 @@ __global__ __launch_bounds__(64 * kFixSlices) void split_fixup_kernel(AttnArgs a
             f32x4 o[FB];
 #pragma unroll
             for (int k = 0; k < FB; ++k) {
-                const int c = c0 + k * n_sl;
-                const int64_t u = u0 + min(c, n - 1);
-                l[k] = c < n ? pl.ws_lse[u * BM + r] : -INFINITY;
-                o[k] = *reinterpret_cast<const f32x4 *>(pl.ws_o + (u * BM + r) * a.D + d);
+                const int c = c0 + k * n_sl;  // wave-uniform
+                if (c < n) {
+                    const int64_t u = u0 + c;
+                    l[k] = pl.ws_lse[u * BM + r];
+                    o[k] = *reinterpret_cast<const f32x4 *>(pl.ws_o + (u * BM + r) * a.D + d);
+                } else {  // past this slice's last unit: weight 0, nothing loaded
+                    l[k] = -INFINITY;
+                    o[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+                }
             }
             float mb = m;
 #pragma unroll
