@@ -65,6 +65,19 @@ def test_cross_plan():
     assert p["workspace_bytes"] == 64 * 128 * 129 * 4
 
 
+def test_paired_leftover_tiles_after_full_rounds_split():
+    """The image context (257 tokens, 5 key tiles): 1032 tiles of 128 rows
+    on 512 slots, the 8 past two rounds split into 5 one-tile ranges; a
+    paired launch that does not fill one round (344 tiles) keeps its tiles
+    whole."""
+    p = attn_plan(1, 12, 10920, 257, 128)
+    check_invariants(p, 1, 12, 10920, 257, 128, 256)
+    assert (p["tile_rows"], p["whole_tiles"], p["split_tiles"], p["key_ranges"]) == (128, 1024, 8, 5)
+    p = attn_plan(1, 4, 10920, 512, 128)
+    check_invariants(p, 1, 4, 10920, 512, 128, 256)
+    assert (p["tile_rows"], p["query_tiles"], p["split_tiles"], p["workspace_bytes"]) == (128, 344, 0, 0)
+
+
 def test_short_underfilled_call_splits():
     """Few 128-row tiles with many keys below the ping-pong threshold: 3
     tiles on 512 slots are split along the keys."""
